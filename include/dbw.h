@@ -1,0 +1,223 @@
+/*
+ * dbw.h -- C ABI of the Dynamic Backup Workers (DBW) hot path on one MI355X.
+ *
+ * The library simulates a synchronous parameter server (PS) with n logical
+ * workers on one GPU (Xu, Neglia, Sebastianelli, "Dynamic Backup Workers for
+ * Parallel Machine Learning", Sect. 2 and Sect. 3):
+ *   - every worker computes a minibatch gradient at the same w_t (Eq. gradient);
+ *   - the PS averages only the k_t fastest gradients (Eq. grad_bw) and updates
+ *     w (Eq. update);
+ *   - DBW picks k_t = n - b_t from end-of-iteration gradient statistics
+ *     (Eqs. sumvariancekt, normsquarekt, estimateL and their D-window means,
+ *     Eq. gain) and from an estimate of the order-statistic arrival times
+ *     (Eq. quadratic_opt), maximising gain per unit of time (Eqs. greedy,
+ *     greedy2).
+ *
+ * Conventions for every entry point:
+ *   - Pointers named as DEVICE are device memory owned by the caller; they are
+ *     read or written asynchronously on the context's HIP stream and must stay
+ *     valid until the stream has passed the call.  HOST pointers are read or
+ *     written before the call returns.
+ *   - Arrays are dense and row-major; float is IEEE fp32, double fp64.
+ *   - Model parameters w have P = dbw_param_count(cfg) floats:
+ *       softmax regression: W [d][C] (no bias), P = d*C;
+ *       MLP d-H-C with ReLU: [W1 (d x H) | b1 (H) | W2 (H x C) | b2 (C)].
+ *     Gradients use the same layout.
+ *   - Every call returns a dbw_status; nothing throws across the ABI.  Argument
+ *     errors are detected on the host before any work is queued (DBW_EINVAL,
+ *     DBW_ERANGE).  Errors only the kernels can see (a minibatch row index
+ *     outside the dataset, k larger than the number of workers that ever
+ *     arrive) raise a device error flag that dbw_sync() reports.  HIP failures
+ *     return DBW_EHIP.  dbw_last_error() gives a text for the last failure.
+ *   - A context is not thread-safe; distinct contexts are independent.
+ */
+#ifndef DBW_H
+#define DBW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DBW_OK = 0,
+  DBW_EINVAL = -1,      /* bad argument: NULL pointer, shape, config        */
+  DBW_ERANGE = -2,      /* k outside [1, n] or beyond the workers that arrive,
+                           row index outside the dataset                     */
+  DBW_EHIP = -3,        /* a HIP runtime call failed                         */
+  DBW_ESTATE = -4,      /* call does not fit the context's state             */
+  DBW_EUNSUPPORTED = -5 /* shape the kernels do not handle                   */
+} dbw_status;
+
+typedef enum { DBW_SOFTMAX = 0, DBW_MLP = 1 } dbw_model;
+
+#define DBW_MAX_N 1024 /* logical workers per context                       */
+#define DBW_MAX_D 64   /* length of the estimator averaging window D          */
+
+/* Problem description.  n workers, minibatch B per worker, d input features,
+ * C classes, H hidden units (MLP only), learning rate eta (constant for all
+ * k), window D of the estimator averages, loss guard factor beta >= 1
+ * (Eq. greedy2).  S > 0 declares a resident dataset of S rows that minibatches
+ * may index (see dbw_worker_grads); S = 0 means minibatches are passed
+ * materialised. */
+typedef struct {
+  int32_t model; /* dbw_model */
+  int32_t n, B, d, C, H;
+  int32_t D;
+  int32_t reserved0;
+  double eta, beta;
+  int64_t S;
+} dbw_config;
+
+/* End-of-iteration statistics over the k received gradients (Sect. 3.1):
+ * gnorm2 = ||g_t||^2; V_plus = Eq. sumvariancekt (for k = 1 the current
+ * D-window mean of past V_plus, 0 without history); N_plus = Eq.
+ * normsquarekt; F_hat = mean minibatch loss of the received workers. */
+typedef struct {
+  double gnorm2, V_plus, N_plus, F_hat;
+} dbw_iter_stats;
+
+/* DBW estimator state carried between iterations (Sect. 3.1, 3.3).  Histories
+ * are oldest first; only the last D entries are kept.  hL holds the
+ * smoothness estimates L_plus (Eq. estimateL), pushed from the second
+ * iteration on when their denominator is positive.  F_prev, F_prev2 are
+ * F_hat of the two previous iterations (nF of them valid). */
+typedef struct {
+  int64_t t;      /* iterations completed                                   */
+  int32_t k_prev; /* k_{t-1}; n before the first iteration                  */
+  int32_t nV;     /* valid entries of hV and hN                              */
+  int32_t nL;     /* valid entries of hL                                     */
+  int32_t nF;     /* valid entries among F_prev, F_prev2 (0..2)              */
+  double F_prev, F_prev2;
+  double hV[DBW_MAX_D], hN[DBW_MAX_D], hL[DBW_MAX_D];
+} dbw_estimator_state;
+
+typedef struct dbw_ctx dbw_ctx;
+
+/* P for a configuration; -1 if the configuration is invalid. */
+int64_t dbw_param_count(const dbw_config* cfg);
+
+/* Create a context bound to HIP stream `stream` (a hipStream_t, NULL for the
+ * default stream) on the current device.  Validates cfg (n in [1, DBW_MAX_N],
+ * B, d, C >= 1, C <= 4096, H >= 1 for the MLP, D in [1, DBW_MAX_D], eta > 0,
+ * beta >= 1, S >= 0), allocates all device workspace (no allocation happens in
+ * later calls) and sets the estimator state to its initial value. */
+dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out);
+void dbw_destroy(dbw_ctx* ctx);
+const char* dbw_last_error(const dbw_ctx* ctx);
+
+/* Waits for the context's stream and reports device-side errors raised since
+ * the last dbw_sync (then clears them): DBW_ERANGE for a row index outside
+ * [0, S) or k beyond the number of workers whose tick is below INT64_MAX. */
+dbw_status dbw_sync(dbw_ctx* ctx);
+
+/* Worker gradients (Sect. 2, Eq. gradient).  For each worker i, at the common
+ * parameters w (DEVICE float [P]):
+ *   G[i] = (1/B) sum_b grad f(x_{i,b}, w)   (DEVICE float [n][P], out)
+ *   loss[i] = (1/B) sum_b f(x_{i,b}, w)      (DEVICE float [n], out)
+ * with f the natural-log cross-entropy of the softmax of the model output.
+ * Minibatches: if rows == NULL, X is DEVICE float [n][B][d] and y DEVICE int32
+ * [n][B]; else X is the resident dataset DEVICE float [S][d], y its labels
+ * DEVICE int32 [S], and rows DEVICE int32 [n][B] lists each worker's row
+ * indices into it.  Labels must lie in [0, C). */
+dbw_status dbw_worker_grads(dbw_ctx* ctx, const float* w, const float* X, const int32_t* y,
+                            const int32_t* rows, float* G, float* loss);
+
+/* Fastest-k aggregation (Sect. 2, Eq. grad_bw).  ticks (DEVICE int64 [n]) are
+ * the round-trip times of the n workers in integer ticks; arrival order is the
+ * order of (tick, worker index).  Writes mask (DEVICE uint8 [n]): 1 for the k
+ * first arrivals, else 0; and g (DEVICE float [P]) = (1/k) sum of their rows
+ * of G (DEVICE float [n][P]).  k (host) must lie in [1, n]. */
+dbw_status dbw_aggregate_fastest(dbw_ctx* ctx, const float* G, const int64_t* ticks, int32_t k,
+                                 float* g, uint8_t* mask);
+
+/* Gradient statistics over the workers with mask[j] = 1 (Sect. 3.1,
+ * Eqs. sumvariancekt, normsquarekt, loss estimate).  G DEVICE float [n][P],
+ * mask DEVICE uint8 [n] with exactly k ones, g DEVICE float [P] their mean,
+ * loss DEVICE float [n].  Writes sqnorm (DEVICE float [n]) = ||G[j]||^2 for
+ * selected j, 0 otherwise, and *stats (DEVICE dbw_iter_stats).  For k = 1
+ * V_plus is the context's current D-window mean of V_plus. */
+dbw_status dbw_grad_stats(dbw_ctx* ctx, const float* G, const uint8_t* mask, int32_t k,
+                          const float* g, const float* loss, float* sqnorm,
+                          dbw_iter_stats* stats);
+
+/* Choice of k_t = n - b_t from the context's estimator state (Sect. 3.3,
+ * Eqs. gain, greedy, greedy2).  T_hat (DEVICE double [n]) holds the time
+ * estimates T_hat_k for k = 1..n; an entry that is not finite and positive
+ * makes that k ineligible.  Writes k_out, b_out (DEVICE int32) and, if not
+ * NULL, objective (DEVICE double [n]) = G_hat_k / T_hat_k (NaN before the
+ * first smoothness estimate exists, and for ineligible k).  The state is not
+ * modified. */
+dbw_status dbw_choose_b(dbw_ctx* ctx, const double* T_hat, int32_t* k_out, int32_t* b_out,
+                        double* objective);
+
+/* One full DBW iteration t: estimate T_hat from the arrival times recorded so
+ * far (host, Eq. quadratic_opt), choose k_t, compute all n worker gradients,
+ * aggregate the k_t first arrivals, compute the statistics, update
+ * w <- w - eta g_t (w DEVICE float [P], in place), and push the estimator
+ * state.  X, y, rows as in dbw_worker_grads.  ticks_host (HOST int64 [n]) are
+ * this iteration's round-trip ticks; they are recorded as samples of row
+ * h = k_{t-1} once k_{t-1} is known, and advance the virtual clock by the
+ * k_t-th smallest tick.  If k_host is not NULL the call waits for the
+ * iteration's choice and stores k_t there; otherwise it returns as soon as the
+ * work is queued. */
+dbw_status dbw_step(dbw_ctx* ctx, float* w, const float* X, const int32_t* y,
+                    const int32_t* rows, const int64_t* ticks_host, int32_t* k_host);
+
+/* Device views of the buffers the last dbw_step wrote (valid until the next
+ * dbw_step on this context): G [n][P], loss [n], g [P], mask [n], sqnorm [n],
+ * stats, T_hat [n], objective [n], k, b. */
+typedef struct {
+  const float* G;
+  const float* loss;
+  const float* g;
+  const uint8_t* mask;
+  const float* sqnorm;
+  const dbw_iter_stats* stats;
+  const double* T_hat;
+  const double* objective;
+  const int32_t* k;
+  const int32_t* b;
+} dbw_step_buffers;
+dbw_status dbw_step_outputs(dbw_ctx* ctx, dbw_step_buffers* out);
+
+/* Estimate of E[T_{k,k}] for k = 1..n (Sect. 3.2, Eq. quadratic_opt); pure
+ * host computation.  cnt and tsum (HOST int64 [n][n], index [h-1][k-1]) are
+ * the number and sum (in ticks) of arrival-time samples of the k-th arrival
+ * when the previous iteration waited for h gradients.  The estimates solve the
+ * constrained least-squares problem exactly; since unsampled cells leave the
+ * solution non-unique, T_hat_k (HOST double [n], out) is the smallest value
+ * x_{k,k} takes in a feasible completion of the optimum (equal to x*_{k,k}
+ * when cell (k,k) was sampled), and NaN when no sampled cell lies below
+ * (k,k).  Returns DBW_EINVAL for n outside [1, DBW_MAX_N], negative counts or
+ * sums, or a sum on a cell with zero count. */
+dbw_status dbw_time_estimate(int32_t n, const int64_t* cnt, const int64_t* tsum, double* T_hat);
+
+/* Estimator state transfer (resume, lockstep testing).  HOST structs; both
+ * calls synchronise the context's stream. */
+dbw_status dbw_state_export(dbw_ctx* ctx, dbw_estimator_state* out);
+dbw_status dbw_state_import(dbw_ctx* ctx, const dbw_estimator_state* in);
+
+/* Arrival-time samples (HOST int64 [n][n] each, as in dbw_time_estimate) and
+ * the virtual clock (HOST int64, ticks).  Export first folds in every
+ * iteration whose row is known (it synchronises the stream). */
+dbw_status dbw_samples_export(dbw_ctx* ctx, int64_t* cnt, int64_t* tsum, int64_t* clock);
+dbw_status dbw_samples_import(dbw_ctx* ctx, const int64_t* cnt, const int64_t* tsum,
+                              int64_t clock);
+
+/* Kernel timing with HIP events on the context's stream.  When enabled, every
+ * launch of the listed kernel groups is bracketed by events; dbw_kernel_time
+ * synchronises and returns the summed milliseconds and the launch count since
+ * the last reset. */
+typedef enum { DBW_KT_GRADS = 0, DBW_KT_AGGREGATE = 1, DBW_KT_CHOOSE = 2, DBW_KT_COUNT = 3 } dbw_kernel_group;
+dbw_status dbw_profile_enable(dbw_ctx* ctx, int32_t on);
+dbw_status dbw_kernel_time(dbw_ctx* ctx, int32_t group, double* total_ms, int64_t* launches);
+dbw_status dbw_profile_reset(dbw_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DBW_H */

@@ -1,0 +1,642 @@
+// C ABI of the DBW library: context, argument checks, workspace, the
+// one-iteration pipeline and the host bookkeeping of arrival times.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <initializer_list>
+#include <limits>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "dbw.h"
+#include "dbw_internal.h"
+
+#define DBW_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+constexpr int kSlots = 4;          // in-flight iterations of the host pipeline
+constexpr int kProfilePairs = 8192;
+
+struct Span {
+  size_t off = 0;
+  size_t bytes = 0;
+};
+
+struct ProfileGroup {
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+  double done_ms = 0.0;
+  int64_t done_launches = 0;
+};
+
+}  // namespace
+
+struct dbw_ctx {
+  dbw_config cfg{};
+  int64_t P = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  std::string last_error;
+  dbw::SoftmaxPlan splan;
+  int64_t agg_nblocks = 0;
+
+  char* pool = nullptr;
+  // device buffers (carved from pool)
+  float* G = nullptr;
+  float* loss = nullptr;
+  float* g = nullptr;
+  uint8_t* mask = nullptr;
+  float* sqnorm = nullptr;
+  dbw_iter_stats* stats = nullptr;
+  double* T_hat = nullptr;
+  double* objective = nullptr;
+  int32_t* k = nullptr;
+  int32_t* b = nullptr;
+  int32_t* sel = nullptr;
+  int64_t* ticks = nullptr;
+  dbw_estimator_state* st = nullptr;
+  int32_t* err = nullptr;
+  float* Gp = nullptr;
+  float* lossp = nullptr;
+  uint32_t* counters = nullptr;
+  float* Z = nullptr;
+  float* ce = nullptr;
+  float* sqpart = nullptr;
+  double* part = nullptr;
+  float* A = nullptr;
+  float* Hh = nullptr;
+  float* dA = nullptr;
+  float* R = nullptr;
+
+  // pinned host staging
+  double* h_T = nullptr;        // [kSlots][n]
+  int64_t* h_ticks = nullptr;   // [kSlots][n]
+  int32_t* h_k = nullptr;       // [kSlots]
+  int32_t* h_err = nullptr;     // [1]
+  hipEvent_t ev[kSlots]{};
+
+  // host bookkeeping of arrival times
+  int64_t t = 0;                // next iteration index (== device state t once drained)
+  int64_t base = 0;             // first iteration issued since create/import
+  int32_t k_prev_base = 0;      // k_{base-1}
+  int64_t recorded = 0;         // iterations whose samples are in the grid
+  int64_t clocked = 0;          // iterations whose k-th arrival advanced the clock
+  std::vector<int64_t> sorted[kSlots];
+  std::vector<int64_t> cnt, tsum;
+  int64_t clock = 0;
+  std::vector<double> T_scratch;
+
+  bool profiling = false;
+  ProfileGroup prof[DBW_KT_COUNT];
+};
+
+namespace {
+
+dbw_status fail(dbw_ctx* c, dbw_status s, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->last_error = buf;
+  }
+  return s;
+}
+
+#define HIP_TRY(ctx, expr)                                                               \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail((ctx), DBW_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));       \
+  } while (0)
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) == hipSuccess && prev != dev) (void)hipSetDevice(dev);
+    else prev = -1;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+bool config_ok(const dbw_config* c, std::string* why) {
+  if (!c) {
+    *why = "config is NULL";
+    return false;
+  }
+  if (c->model != DBW_SOFTMAX && c->model != DBW_MLP) *why = "model must be DBW_SOFTMAX or DBW_MLP";
+  else if (c->n < 1 || c->n > DBW_MAX_N) *why = "n outside [1, DBW_MAX_N]";
+  else if (c->B < 1 || c->d < 1) *why = "B and d must be >= 1";
+  else if (c->C < 2 || c->C > 4096) *why = "C outside [2, 4096]";
+  else if (c->model == DBW_MLP && (c->H < 1 || c->H > 65536)) *why = "H outside [1, 65536]";
+  else if (c->D < 1 || c->D > DBW_MAX_D) *why = "D outside [1, DBW_MAX_D]";
+  else if (!(c->eta > 0.0) || !std::isfinite(c->eta)) *why = "eta must be finite and > 0";
+  else if (!(c->beta >= 1.0) || !std::isfinite(c->beta)) *why = "beta must be finite and >= 1";
+  else if (c->S < 0 || c->S > (int64_t{1} << 31)) *why = "S outside [0, 2^31]";
+  else if ((int64_t)c->n * c->B > (int64_t{1} << 30)) *why = "n*B too large";
+  else return true;
+  return false;
+}
+
+int64_t param_count(const dbw_config& c) {
+  if (c.model == DBW_SOFTMAX) return (int64_t)c.d * c.C;
+  return (int64_t)c.d * c.H + c.H + (int64_t)c.H * c.C + c.C;
+}
+
+void reset_host_pipeline(dbw_ctx* c, int64_t t, int32_t k_prev) {
+  c->t = c->base = c->recorded = c->clocked = t;
+  c->k_prev_base = k_prev;
+}
+
+// k_u for an issued iteration u (waits for the iteration's choice).
+dbw_status known_k(dbw_ctx* c, int64_t u, int32_t* k) {
+  if (u < c->base) {
+    if (u == c->base - 1) {
+      *k = c->k_prev_base;
+      return DBW_OK;
+    }
+    return fail(c, DBW_ESTATE, "iteration %lld precedes the context's history", (long long)u);
+  }
+  const int slot = static_cast<int>(u % kSlots);
+  HIP_TRY(c, hipEventSynchronize(c->ev[slot]));
+  *k = c->h_k[slot];
+  return DBW_OK;
+}
+
+// Fold into the grid every iteration u < upto whose row k_{u-1} is known, and
+// into the clock every iteration u < clock_upto.
+dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
+  const int n = c->cfg.n;
+  while (c->recorded < upto) {
+    const int64_t u = c->recorded;
+    int32_t h;
+    dbw_status s = known_k(c, u - 1, &h);
+    if (s != DBW_OK) return s;
+    const std::vector<int64_t>& srt = c->sorted[u % kSlots];
+    for (int i = 0; i < n; ++i) {
+      c->cnt[(size_t)(h - 1) * n + i] += 1;
+      c->tsum[(size_t)(h - 1) * n + i] += srt[i];
+    }
+    c->recorded++;
+  }
+  while (c->clocked < clock_upto) {
+    const int64_t u = c->clocked;
+    int32_t k;
+    dbw_status s = known_k(c, u, &k);
+    if (s != DBW_OK) return s;
+    c->clock += c->sorted[u % kSlots][k - 1];
+    c->clocked++;
+  }
+  return DBW_OK;
+}
+
+dbw_status check_device_ptrs(dbw_ctx* c, std::initializer_list<std::pair<const void*, const char*>> ps) {
+  for (auto& p : ps)
+    if (!p.first) return fail(c, DBW_EINVAL, "%s is NULL", p.second);
+  return DBW_OK;
+}
+
+struct ProfScope {
+  dbw_ctx* c;
+  int g;
+  bool on;
+  ProfScope(dbw_ctx* ctx, int group) : c(ctx), g(group) {
+    ProfileGroup& pg = c->prof[g];
+    on = c->profiling && pg.used < static_cast<int>(pg.start.size());
+    if (on) (void)hipEventRecord(pg.start[pg.used], c->stream);
+  }
+  ~ProfScope() {
+    if (on) {
+      ProfileGroup& pg = c->prof[g];
+      (void)hipEventRecord(pg.stop[pg.used], c->stream);
+      pg.used++;
+    }
+  }
+};
+
+dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_t* y, const int32_t* rows,
+                        float* G, float* loss) {
+  ProfScope ps(c, DBW_KT_GRADS);
+  const dbw_config& cf = c->cfg;
+  hipError_t e;
+  if (cf.model == DBW_SOFTMAX) {
+    dbw::SoftmaxArgs a{};
+    a.W = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
+    a.n = cf.n; a.B = cf.B; a.d = cf.d; a.C = cf.C;
+    a.G = G; a.loss = loss;
+    a.Gp = c->Gp; a.lossp = c->lossp; a.counters = c->counters; a.Z = c->Z; a.ce = c->ce;
+    a.err = c->err;
+    e = dbw::launch_softmax_grads(c->splan, a, c->stream);
+  } else {
+    dbw::MlpArgs a{};
+    a.w = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
+    a.n = cf.n; a.B = cf.B; a.d = cf.d; a.H = cf.H; a.C = cf.C;
+    a.G = G; a.loss = loss;
+    a.A = c->A; a.Hh = c->Hh; a.dA = c->dA; a.R = c->R; a.ce = c->ce; a.err = c->err;
+    e = dbw::launch_mlp_grads(a, c->stream);
+  }
+  if (e != hipSuccess) return fail(c, DBW_EHIP, "gradient kernels: %s", hipGetErrorString(e));
+  return DBW_OK;
+}
+
+dbw_status check_batch(dbw_ctx* c, const float* X, const int32_t* y, const int32_t* rows) {
+  if (!X || !y) return fail(c, DBW_EINVAL, "X and y must be non-NULL");
+  if (rows && c->cfg.S <= 0) return fail(c, DBW_EINVAL, "row indices need a dataset: create the context with S > 0");
+  return DBW_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+DBW_API int64_t dbw_param_count(const dbw_config* cfg) {
+  std::string why;
+  if (!config_ok(cfg, &why)) return -1;
+  return param_count(*cfg);
+}
+
+DBW_API const char* dbw_last_error(const dbw_ctx* ctx) { return ctx ? ctx->last_error.c_str() : "NULL context"; }
+
+DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out) {
+  if (!out) return DBW_EINVAL;
+  *out = nullptr;
+  std::string why;
+  if (!config_ok(cfg, &why)) return DBW_EINVAL;
+  dbw_ctx* c = new (std::nothrow) dbw_ctx();
+  if (!c) return DBW_EINVAL;
+  c->cfg = *cfg;
+  c->P = param_count(*cfg);
+  c->stream = static_cast<hipStream_t>(stream);
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return DBW_EHIP;
+  }
+  const dbw_config& cf = c->cfg;
+  const int64_t n = cf.n, P = c->P, rowsN = (int64_t)cf.n * cf.B;
+  if (cf.model == DBW_SOFTMAX) c->splan = dbw::softmax_plan(cf.n, cf.B, cf.d, cf.C);
+  c->agg_nblocks = dbw::agg_blocks(P);
+
+  // workspace layout
+  std::vector<Span> spans;
+  size_t total = 0;
+  auto take = [&](size_t bytes) {
+    Span s;
+    s.off = total;
+    s.bytes = bytes;
+    total += (bytes + 255) / 256 * 256;
+    return s;
+  };
+  Span sG = take(sizeof(float) * n * P), sLoss = take(sizeof(float) * n), sg = take(sizeof(float) * P),
+       sMask = take(n), sSq = take(sizeof(float) * n), sStats = take(sizeof(dbw_iter_stats)),
+       sT = take(sizeof(double) * n), sObj = take(sizeof(double) * n), sK = take(4), sB = take(4),
+       sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
+       sSt = take(sizeof(dbw_estimator_state)), sErr = take(4),
+       sSqp = take(sizeof(float) * n * c->agg_nblocks), sPart = take(sizeof(double) * 2 * c->agg_nblocks);
+  Span sGp, sLp, sCnt, sZ, sCe, sA, sH, sdA, sR;
+  if (cf.model == DBW_SOFTMAX) {
+    if (c->splan.fused) {
+      if (c->splan.slabs > 1) {
+        sGp = take(sizeof(float) * n * c->splan.slabs * P);
+        sLp = take(sizeof(float) * n * c->splan.slabs);
+      }
+      sCnt = take(sizeof(uint32_t) * n);
+    } else {
+      sZ = take(sizeof(float) * rowsN * cf.C);
+      sCe = take(sizeof(float) * rowsN);
+    }
+  } else {
+    sA = take(sizeof(float) * rowsN * cf.H);
+    sH = take(sizeof(float) * rowsN * cf.H);
+    sdA = take(sizeof(float) * rowsN * cf.H);
+    sR = take(sizeof(float) * rowsN * cf.C);
+    sCe = take(sizeof(float) * rowsN);
+  }
+  if (hipMalloc(&c->pool, total) != hipSuccess) {
+    delete c;
+    return DBW_EHIP;
+  }
+  auto at = [&](const Span& s) -> void* { return s.bytes ? c->pool + s.off : nullptr; };
+  c->G = (float*)at(sG); c->loss = (float*)at(sLoss); c->g = (float*)at(sg); c->mask = (uint8_t*)at(sMask);
+  c->sqnorm = (float*)at(sSq); c->stats = (dbw_iter_stats*)at(sStats); c->T_hat = (double*)at(sT);
+  c->objective = (double*)at(sObj); c->k = (int32_t*)at(sK); c->b = (int32_t*)at(sB);
+  c->sel = (int32_t*)at(sSel); c->ticks = (int64_t*)at(sTicks); c->st = (dbw_estimator_state*)at(sSt);
+  c->err = (int32_t*)at(sErr); c->sqpart = (float*)at(sSqp); c->part = (double*)at(sPart);
+  c->Gp = (float*)at(sGp); c->lossp = (float*)at(sLp); c->counters = (uint32_t*)at(sCnt);
+  c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->A = (float*)at(sA); c->Hh = (float*)at(sH);
+  c->dA = (float*)at(sdA); c->R = (float*)at(sR);
+
+  bool ok = hipMemset(c->pool, 0, total) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_T, sizeof(double) * kSlots * n, hipHostMallocDefault) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_ticks, sizeof(int64_t) * kSlots * n, hipHostMallocDefault) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_k, sizeof(int32_t) * kSlots, hipHostMallocDefault) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
+  for (int s = 0; s < kSlots && ok; ++s) ok = hipEventCreateWithFlags(&c->ev[s], hipEventDisableTiming) == hipSuccess;
+  if (!ok) {
+    dbw_destroy(c);
+    return DBW_EHIP;
+  }
+  dbw_estimator_state init{};
+  init.t = 0;
+  init.k_prev = cf.n;
+  ok = hipMemcpy(c->st, &init, sizeof init, hipMemcpyHostToDevice) == hipSuccess;
+  ok = ok && hipDeviceSynchronize() == hipSuccess;
+  if (!ok) {
+    dbw_destroy(c);
+    return DBW_EHIP;
+  }
+  c->cnt.assign((size_t)n * n, 0);
+  c->tsum.assign((size_t)n * n, 0);
+  for (auto& v : c->sorted) v.assign(n, 0);
+  c->T_scratch.assign(n, 0.0);
+  reset_host_pipeline(c, 0, cf.n);
+  *out = c;
+  return DBW_OK;
+}
+
+DBW_API void dbw_destroy(dbw_ctx* c) {
+  if (!c) return;
+  DeviceGuard g(c->device);
+  if (c->stream || c->pool) (void)hipStreamSynchronize(c->stream);
+  for (auto& ev : c->ev)
+    if (ev) (void)hipEventDestroy(ev);
+  for (auto& pg : c->prof) {
+    for (auto e : pg.start) (void)hipEventDestroy(e);
+    for (auto e : pg.stop) (void)hipEventDestroy(e);
+  }
+  if (c->h_T) (void)hipHostFree(c->h_T);
+  if (c->h_ticks) (void)hipHostFree(c->h_ticks);
+  if (c->h_k) (void)hipHostFree(c->h_k);
+  if (c->h_err) (void)hipHostFree(c->h_err);
+  if (c->pool) (void)hipFree(c->pool);
+  delete c;
+}
+
+DBW_API dbw_status dbw_sync(dbw_ctx* c) {
+  if (!c) return DBW_EINVAL;
+  DeviceGuard g(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(c->h_err, c->err, sizeof(int32_t), hipMemcpyDeviceToHost));
+  const int32_t e = *c->h_err;
+  if (e) {
+    *c->h_err = 0;
+    HIP_TRY(c, hipMemcpy(c->err, c->h_err, sizeof(int32_t), hipMemcpyHostToDevice));
+    std::string msg = "device reported:";
+    if (e & dbw::ERR_ROW_RANGE) msg += " row index outside [0, S);";
+    if (e & dbw::ERR_K_RANGE) msg += " k exceeds the workers that arrive;";
+    if (e & dbw::ERR_LABEL_RANGE) msg += " label outside [0, C);";
+    if (e & dbw::ERR_MASK_COUNT) msg += " mask does not hold k ones;";
+    return fail(c, (e & (dbw::ERR_LABEL_RANGE | dbw::ERR_MASK_COUNT)) && !(e & (dbw::ERR_ROW_RANGE | dbw::ERR_K_RANGE))
+                       ? DBW_EINVAL : DBW_ERANGE, "%s", msg.c_str());
+  }
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_worker_grads(dbw_ctx* c, const float* w, const float* X, const int32_t* y,
+                                    const int32_t* rows, float* G, float* loss) {
+  if (!c) return DBW_EINVAL;
+  if (dbw_status s = check_device_ptrs(c, {{w, "w"}, {G, "G"}, {loss, "loss"}}); s != DBW_OK) return s;
+  if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
+  DeviceGuard g(c->device);
+  return launch_grads(c, w, X, y, rows, G, loss);
+}
+
+DBW_API dbw_status dbw_aggregate_fastest(dbw_ctx* c, const float* G, const int64_t* ticks, int32_t k, float* g,
+                                         uint8_t* mask) {
+  if (!c) return DBW_EINVAL;
+  if (dbw_status s = check_device_ptrs(c, {{G, "G"}, {ticks, "ticks"}, {g, "g"}, {mask, "mask"}}); s != DBW_OK)
+    return s;
+  if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
+  DeviceGuard dg(c->device);
+  ProfScope ps(c, DBW_KT_AGGREGATE);
+  dbw::ChooseArgs ca{};
+  ca.ticks = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
+  ca.sel = c->sel; ca.mask = mask; ca.err = c->err;
+  HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+  dbw::AggArgs aa{};
+  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.sel = c->sel; aa.k_imm = k; aa.g_out = g;
+  aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_MEAN;
+  HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_grad_stats(dbw_ctx* c, const float* G, const uint8_t* mask, int32_t k, const float* g,
+                                  const float* loss, float* sqnorm, dbw_iter_stats* stats) {
+  if (!c) return DBW_EINVAL;
+  if (dbw_status s = check_device_ptrs(
+          c, {{G, "G"}, {mask, "mask"}, {g, "g"}, {loss, "loss"}, {sqnorm, "sqnorm"}, {stats, "stats"}});
+      s != DBW_OK)
+    return s;
+  if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
+  DeviceGuard dg(c->device);
+  ProfScope ps(c, DBW_KT_AGGREGATE);
+  HIP_TRY(c, dbw::launch_mask_to_sel(mask, c->cfg.n, k, c->sel, c->err, c->stream));
+  dbw::AggArgs aa{};
+  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.sel = c->sel; aa.k_imm = k; aa.g_in = g;
+  aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_STATS_GIVEN_MEAN;
+  HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+  dbw::FinalizeArgs fa{};
+  fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = mask; fa.k_imm = k;
+  fa.loss = loss; fa.n = c->cfg.n; fa.sqnorm = sqnorm; fa.stats = stats; fa.st = c->st;
+  fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 0; fa.err = c->err;
+  HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_choose_b(dbw_ctx* c, const double* T_hat, int32_t* k_out, int32_t* b_out,
+                                double* objective) {
+  if (!c) return DBW_EINVAL;
+  if (dbw_status s = check_device_ptrs(c, {{T_hat, "T_hat"}, {k_out, "k_out"}, {b_out, "b_out"}}); s != DBW_OK)
+    return s;
+  DeviceGuard dg(c->device);
+  ProfScope ps(c, DBW_KT_CHOOSE);
+  dbw::ChooseArgs ca{};
+  ca.st = c->st; ca.T_hat = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
+  ca.do_choose = 1; ca.do_select = 0; ca.k_out = k_out; ca.b_out = b_out; ca.objective = objective;
+  ca.err = c->err;
+  HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t* y, const int32_t* rows,
+                            const int64_t* ticks_host, int32_t* k_host) {
+  if (!c) return DBW_EINVAL;
+  if (dbw_status s = check_device_ptrs(c, {{w, "w"}}); s != DBW_OK) return s;
+  if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
+  if (!ticks_host) return fail(c, DBW_EINVAL, "ticks_host is NULL");
+  const int n = c->cfg.n;
+  for (int i = 0; i < n; ++i)
+    if (ticks_host[i] < 0) return fail(c, DBW_EINVAL, "tick of worker %d is negative", i);
+  DeviceGuard dg(c->device);
+  const int64_t t = c->t;
+  const int slot = static_cast<int>(t % kSlots);
+  // 1. arrival times of iterations up to t-1 into the grid (needs k_{t-2}),
+  //    clock through iteration t-2.
+  if (dbw_status s = fold(c, t, std::max<int64_t>(c->clocked, t - 1)); s != DBW_OK) return s;
+  // the slot's previous user (iteration t - kSlots) has drained: its event
+  // was waited for above (k_{t-2} is newer).
+  // 2. time estimate T_hat_t on the host
+  std::string why;
+  double* hT = c->h_T + (size_t)slot * n;
+  if (dbw::time_estimate(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
+    return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  int64_t* hk = c->h_ticks + (size_t)slot * n;
+  std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
+  std::vector<int64_t>& srt = c->sorted[slot];
+  srt.assign(ticks_host, ticks_host + n);
+  std::sort(srt.begin(), srt.end());
+  HIP_TRY(c, hipMemcpyAsync(c->T_hat, hT, sizeof(double) * n, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(c->ticks, hk, sizeof(int64_t) * n, hipMemcpyHostToDevice, c->stream));
+  // 3. choose k_t and select the first k_t arrivals
+  {
+    ProfScope ps(c, DBW_KT_CHOOSE);
+    dbw::ChooseArgs ca{};
+    ca.st = c->st; ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.n = n; ca.eta = c->cfg.eta;
+    ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
+    ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
+    HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+  }
+  // 4. worker gradients
+  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, c->loss); s != DBW_OK) return s;
+  // 5. aggregate, statistics, update, estimator bookkeeping
+  {
+    ProfScope ps(c, DBW_KT_AGGREGATE);
+    dbw::AggArgs aa{};
+    aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;
+    aa.eta = static_cast<float>(c->cfg.eta); aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_FUSED;
+    HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+    dbw::FinalizeArgs fa{};
+    fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = c->mask; fa.k_dev = c->k;
+    fa.loss = c->loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;
+    fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
+    HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
+  }
+  // 6. k_t back to the host for the arrival-time bookkeeping
+  HIP_TRY(c, hipMemcpyAsync(c->h_k + slot, c->k, sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipEventRecord(c->ev[slot], c->stream));
+  c->t = t + 1;
+  if (k_host) {
+    HIP_TRY(c, hipEventSynchronize(c->ev[slot]));
+    *k_host = c->h_k[slot];
+  }
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_step_outputs(dbw_ctx* c, dbw_step_buffers* out) {
+  if (!c || !out) return DBW_EINVAL;
+  out->G = c->G; out->loss = c->loss; out->g = c->g; out->mask = c->mask; out->sqnorm = c->sqnorm;
+  out->stats = c->stats; out->T_hat = c->T_hat; out->objective = c->objective; out->k = c->k; out->b = c->b;
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_time_estimate(int32_t n, const int64_t* cnt, const int64_t* tsum, double* T_hat) {
+  if (!cnt || !tsum || !T_hat) return DBW_EINVAL;
+  std::string why;
+  return dbw::time_estimate(n, cnt, tsum, T_hat, &why) == 0 ? DBW_OK : DBW_EINVAL;
+}
+
+DBW_API dbw_status dbw_state_export(dbw_ctx* c, dbw_estimator_state* out) {
+  if (!c || !out) return DBW_EINVAL;
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(out, c->st, sizeof *out, hipMemcpyDeviceToHost));
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_state_import(dbw_ctx* c, const dbw_estimator_state* in) {
+  if (!c || !in) return DBW_EINVAL;
+  const dbw_config& cf = c->cfg;
+  if (in->t < 0 || in->k_prev < 1 || in->k_prev > cf.n || in->nV < 0 || in->nV > cf.D || in->nL < 0 ||
+      in->nL > cf.D || in->nF < 0 || in->nF > 2)
+    return fail(c, DBW_EINVAL, "estimator state out of range for this configuration");
+  if ((in->t == 0) != (in->nV == 0) || in->nF > in->t || in->nV > in->t)
+    return fail(c, DBW_EINVAL, "estimator state histories do not match t");
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  // fold what is known before the history restarts
+  if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
+  HIP_TRY(c, hipMemcpy(c->st, in, sizeof *in, hipMemcpyHostToDevice));
+  reset_host_pipeline(c, in->t, in->k_prev);
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_samples_export(dbw_ctx* c, int64_t* cnt, int64_t* tsum, int64_t* clock) {
+  if (!c || !cnt || !tsum || !clock) return DBW_EINVAL;
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
+  std::memcpy(cnt, c->cnt.data(), sizeof(int64_t) * c->cnt.size());
+  std::memcpy(tsum, c->tsum.data(), sizeof(int64_t) * c->tsum.size());
+  *clock = c->clock;
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int64_t* tsum, int64_t clock) {
+  if (!c || !cnt || !tsum) return DBW_EINVAL;
+  const int n = c->cfg.n;
+  std::vector<double> probe(n);
+  std::string why;
+  if (dbw::time_estimate(n, cnt, tsum, probe.data(), &why) != 0)
+    return fail(c, DBW_EINVAL, "samples: %s", why.c_str());
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
+  std::memcpy(c->cnt.data(), cnt, sizeof(int64_t) * c->cnt.size());
+  std::memcpy(c->tsum.data(), tsum, sizeof(int64_t) * c->tsum.size());
+  c->clock = clock;
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
+  if (!c) return DBW_EINVAL;
+  DeviceGuard dg(c->device);
+  if (on) {
+    for (auto& pg : c->prof)
+      while (static_cast<int>(pg.start.size()) < kProfilePairs) {
+        hipEvent_t a, b;
+        HIP_TRY(c, hipEventCreate(&a));
+        HIP_TRY(c, hipEventCreate(&b));
+        pg.start.push_back(a);
+        pg.stop.push_back(b);
+      }
+  }
+  c->profiling = on != 0;
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_kernel_time(dbw_ctx* c, int32_t group, double* total_ms, int64_t* launches) {
+  if (!c || !total_ms || !launches || group < 0 || group >= DBW_KT_COUNT) return DBW_EINVAL;
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  ProfileGroup& pg = c->prof[group];
+  for (int i = 0; i < pg.used; ++i) {
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, pg.start[i], pg.stop[i]));
+    pg.done_ms += ms;
+  }
+  pg.done_launches += pg.used;
+  pg.used = 0;
+  *total_ms = pg.done_ms;
+  *launches = pg.done_launches;
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_profile_reset(dbw_ctx* c) {
+  if (!c) return DBW_EINVAL;
+  DeviceGuard dg(c->device);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (auto& pg : c->prof) {
+    pg.used = 0;
+    pg.done_ms = 0.0;
+    pg.done_launches = 0;
+  }
+  return DBW_OK;
+}

@@ -1,0 +1,149 @@
+// Internal declarations of the DBW library: device workspace layout, kernel
+// launchers and the host time estimator.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "dbw.h"
+
+namespace dbw {
+
+// Device error flags (OR-ed by kernels, read and cleared by dbw_sync).
+enum : int32_t {
+  ERR_ROW_RANGE = 1,    // minibatch row index outside [0, S)
+  ERR_K_RANGE = 2,      // k larger than the number of workers that arrive
+  ERR_LABEL_RANGE = 4,  // label outside [0, C)
+  ERR_MASK_COUNT = 8,   // mask does not hold exactly k ones
+};
+
+// Column tile of the aggregation kernel: 64 lanes x 4 columns.
+constexpr int AGG_TILE = 256;
+constexpr int AGG_WAVES = 4;
+
+inline int64_t agg_blocks(int64_t P) { return (P + AGG_TILE - 1) / AGG_TILE; }
+
+// ---------------------------------------------------------------------------
+// Worker-gradient plans.
+struct SoftmaxPlan {
+  int fused = 0;          // 1: single-pass kernel (small C); 0: GEMM path
+  int threads = 0;        // fused: threads per block
+  int per_thread = 0;     // fused: d-elements per thread (M)
+  int cpad = 0;           // fused: class template (>= C)
+  int slabs = 1;          // fused: row slabs per worker
+  int rows_per_slab = 0;
+};
+
+struct MlpPlan {
+  int ok = 0;
+};
+
+// Softmax regression: G = per-worker gradient of the mean CE of softmax(X W).
+struct SoftmaxArgs {
+  const float* W;        // [d][C]
+  const float* X;        // [n*B][d] or dataset [S][d]
+  const int32_t* y;      // [n*B] or [S]
+  const int32_t* rows;   // nullable [n*B]
+  int64_t S;
+  int n, B, d, C;
+  float* G;              // [n][d*C]
+  float* loss;           // [n]
+  // workspace
+  float* Gp;             // [n*slabs][d*C] slab partials (fused, slabs > 1)
+  float* lossp;          // [n*slabs]
+  uint32_t* counters;    // [n], zero between launches
+  float* Z;              // [n*B][C] logits / residuals (GEMM path)
+  float* ce;             // [n*B] per-row CE (GEMM path)
+  int32_t* err;
+};
+
+SoftmaxPlan softmax_plan(int n, int B, int d, int C);
+hipError_t launch_softmax_grads(const SoftmaxPlan& plan, const SoftmaxArgs& a, hipStream_t s);
+
+struct MlpArgs {
+  const float* w;        // [P] flat parameters
+  const float* X;
+  const int32_t* y;
+  const int32_t* rows;
+  int64_t S;
+  int n, B, d, H, C;
+  float* G;              // [n][P]
+  float* loss;           // [n]
+  // workspace
+  float* A;              // [n*B][H] hidden pre-activations
+  float* Hh;             // [n*B][H] hidden activations
+  float* dA;             // [n*B][H] gradient w.r.t. pre-activations
+  float* R;              // [n*B][C] softmax residual (P - Y)/B
+  float* ce;             // [n*B]
+  int32_t* err;
+};
+hipError_t launch_mlp_grads(const MlpArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// PS side.
+struct ChooseArgs {
+  const dbw_estimator_state* st;  // device
+  const double* T_hat;            // device [n] (choose)
+  const int64_t* ticks;           // device [n] (select)
+  int n;
+  double eta, beta;
+  int do_choose, do_select;
+  int k_imm;                      // k when not choosing
+  int32_t* k_out;                 // device (choose) -- also read by select
+  int32_t* b_out;
+  double* objective;              // nullable
+  int32_t* sel;                   // device [n] arrival-ordered selection
+  uint8_t* mask;                  // device [n]
+  int32_t* err;
+};
+hipError_t launch_choose_select(const ChooseArgs& a, hipStream_t s);
+
+enum AggMode { AGG_MEAN = 0, AGG_STATS_GIVEN_MEAN = 1, AGG_FUSED = 2 };
+struct AggArgs {
+  const float* G;       // [n][P]
+  int64_t P;
+  int n;
+  const int32_t* sel;   // arrival order; AGG_STATS_GIVEN_MEAN uses sel from the mask
+  const int32_t* k_dev; // nullable -> k_imm
+  int k_imm;
+  const float* g_in;    // AGG_STATS_GIVEN_MEAN
+  float* g_out;         // AGG_MEAN, AGG_FUSED
+  float* w;             // AGG_FUSED: updated in place (nullable: no update)
+  float eta;
+  float* sqpart;        // [n][nblocks]
+  double* part;         // [nblocks][2]
+  int mode;
+};
+hipError_t launch_aggregate(const AggArgs& a, hipStream_t s);
+
+struct FinalizeArgs {
+  const float* sqpart;  // [n][nblocks]
+  const double* part;   // [nblocks][2]
+  int64_t nblocks;
+  const uint8_t* mask;  // [n]
+  const int32_t* k_dev; // nullable -> k_imm
+  int k_imm;
+  const float* loss;    // [n]
+  int n;
+  float* sqnorm;        // [n]
+  dbw_iter_stats* stats;
+  dbw_estimator_state* st;  // device; read (window mean), written if bookkeeping
+  double eta;
+  int D;
+  int bookkeeping;
+  int32_t* err;
+};
+hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
+
+// Mask -> arrival-order-free selection list (worker order) for the stats call.
+hipError_t launch_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel, int32_t* err,
+                              hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Host time estimator (exact constrained least squares).
+int time_estimate(int n, const int64_t* cnt, const int64_t* tsum, double* T_hat, std::string* why);
+
+}  // namespace dbw

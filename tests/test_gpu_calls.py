@@ -1,0 +1,258 @@
+"""GPU parity of the four per-call entry points against the oracle:
+dbw_worker_grads (Sect. 2, Eq. gradient), dbw_aggregate_fastest (Eq.
+grad_bw), dbw_grad_stats (Eqs. sumvariancekt, normsquarekt) and dbw_choose_b
+(Eqs. gain, greedy, greedy2).  Tolerance: max relative error 1e-4 for fp32
+gradients and statistics; masks and k bit-exact (k up to objective ties
+within 1e-6)."""
+import numpy as np
+import pytest
+
+from oracle import dbw as odbw
+from oracle import model as omodel
+from oracle import ps as ops
+
+from gpu_util import RTOL, host, k_acceptable, rel_err, scalar_rel, softmax_inputs, to_dev
+
+torch = pytest.importorskip("torch")
+pb = pytest.importorskip("paper_2004_14696_amd.binding")
+
+pytestmark = pytest.mark.gpu
+
+
+def _ctx(n, B, d, C, S=0, model="softmax", H=0, D=5):
+    return pb.Context(pb.make_config(model, n, B, d, C, H=H, D=D, S=S))
+
+
+def _ctx_for_P(n, P, D=5):
+    """A softmax context whose parameter count is P (only P matters for the
+    aggregation and statistics calls)."""
+    C = next(c for c in range(2, 4097) if P % c == 0)
+    return _ctx(n, 1, P // C, C, D=D)
+
+
+SOFTMAX_SHAPES = [
+    # (n, B, d, C): the workload shapes, ragged tiles, both kernels
+    (4, 32, 784, 10),      # 4 workers x 32 rows, 28x28 inputs
+    (16, 128, 784, 10),    # 16 x 128, 28x28
+    (64, 256, 3072, 10),   # 64 x 256, 32x32x3 inputs
+    (1, 1, 1, 2),
+    (3, 7, 100, 3),
+    (5, 13, 1000, 10),
+    (7, 33, 777, 5),
+    (2, 9, 3000, 16),
+    (2, 10, 4500, 10),     # d beyond the fused kernel: GEMM path
+    (4, 24, 300, 100),     # 100 classes: GEMM path
+    (3, 70, 129, 17),      # GEMM path, ragged tiles
+]
+
+
+@pytest.mark.parametrize("n,B,d,C", SOFTMAX_SHAPES)
+def test_worker_grads_softmax(n, B, d, C):
+    rng = np.random.default_rng(1000 + n * 7 + d)
+    X, y, W, _ = softmax_inputs(rng, n, B, d, C)
+    ctx = _ctx(n, B, d, C)
+    G, loss = ctx.worker_grads(to_dev(torch, W), to_dev(torch, X), to_dev(torch, y))
+    ctx.sync()
+    Go, lo = omodel.softmax_worker_grads(W.astype(np.float64), X, y, C)
+    assert rel_err(host(G), Go) <= RTOL
+    for i in range(n):
+        assert rel_err(host(G)[i], Go[i]) <= RTOL
+    assert rel_err(host(loss), lo) <= RTOL
+
+
+@pytest.mark.parametrize("n,B,d,C,S", [(4, 32, 784, 10, 500), (6, 40, 3072, 10, 300), (3, 20, 200, 100, 90)])
+def test_worker_grads_gather_equals_materialised(n, B, d, C, S):
+    rng = np.random.default_rng(77 + d)
+    X, y, W, idx = softmax_inputs(rng, n, B, d, C, S=S)
+    ctx = _ctx(n, B, d, C, S=S)
+    Wd = to_dev(torch, W)
+    G1, l1 = ctx.worker_grads(Wd, to_dev(torch, X), to_dev(torch, y), rows=to_dev(torch, idx))
+    G2, l2 = ctx.worker_grads(Wd, to_dev(torch, X[idx]), to_dev(torch, y[idx]))
+    ctx.sync()
+    assert torch.equal(G1, G2) and torch.equal(l1, l2)
+    Go, _ = omodel.softmax_worker_grads(W.astype(np.float64), X[idx], y[idx], C)
+    assert rel_err(host(G1), Go) <= RTOL
+
+
+def test_worker_grads_largest_softmax_sampled_workers():
+    # 256 workers x 512 rows, 3072 features, 100 classes, minibatches gathered
+    # from a resident 50000-row dataset; the oracle recomputes sampled workers.
+    n, B, d, C, S = 256, 512, 3072, 100, 50000
+    rng = np.random.default_rng(5)
+    X, y, W, idx = softmax_inputs(rng, n, B, d, C, S=S)
+    ctx = _ctx(n, B, d, C, S=S)
+    G, loss = ctx.worker_grads(to_dev(torch, W), to_dev(torch, X), to_dev(torch, y), rows=to_dev(torch, idx))
+    ctx.sync()
+    for i in (0, 131, 255):
+        Go, lo = omodel.softmax_worker_grads(W.astype(np.float64), X[idx[i]][None], y[idx[i]][None], C)
+        assert rel_err(host(G[i]), Go[0]) <= RTOL
+        assert scalar_rel(host(loss)[i], lo[0]) <= RTOL
+
+
+def test_worker_grads_rejects_bad_rows_and_labels():
+    n, B, d, C, S = 2, 4, 16, 3, 10
+    rng = np.random.default_rng(9)
+    X, y, W, idx = softmax_inputs(rng, n, B, d, C, S=S)
+    ctx = _ctx(n, B, d, C, S=S)
+    bad = idx.copy()
+    bad[1, 2] = S + 5                          # outside the dataset
+    ctx.worker_grads(to_dev(torch, W), to_dev(torch, X), to_dev(torch, y), rows=to_dev(torch, bad))
+    with pytest.raises(pb.DBWError) as e:
+        ctx.sync()
+    assert e.value.status == pb.DBW_ERANGE
+    ctx.sync()                                  # the flag is cleared
+    yb = y.copy()
+    yb[3] = C                                   # label outside [0, C)
+    ctx.worker_grads(to_dev(torch, W), to_dev(torch, X), to_dev(torch, yb), rows=to_dev(torch, idx))
+    with pytest.raises(pb.DBWError):
+        ctx.sync()
+    with pytest.raises(ValueError):             # shape checked before any launch
+        ctx.worker_grads(to_dev(torch, W[:-1]), to_dev(torch, X), to_dev(torch, y), rows=to_dev(torch, idx))
+
+
+# -- aggregation --------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,P", [(4, 7840), (16, 7840), (64, 30720), (5, 1001), (33, 259), (256, 4096)])
+def test_aggregate_fastest(n, P):
+    rng = np.random.default_rng(n * 31 + P)
+    G = rng.standard_normal((n, P)).astype(np.float32)
+    ticks = rng.integers(1, max(3, n // 2), size=n).astype(np.int64)    # ties on purpose
+    ctx = _ctx_for_P(n, P)
+    assert ctx.P == P
+    Gd, td = to_dev(torch, G), to_dev(torch, ticks)
+    for k in sorted({1, 2, max(1, n // 2), n - 1 if n > 1 else 1, n}):
+        g, mask = ctx.aggregate_fastest(Gd, td, k)
+        ctx.sync()
+        sel, mo = ops.select_fastest(ticks, k)
+        assert np.array_equal(host(mask), mo), k
+        assert rel_err(host(g), ops.aggregate(G, sel)) <= 1e-5, k
+
+
+def test_aggregate_rejects_bad_k_and_dead_workers():
+    n, P = 6, 64
+    ctx = _ctx(n, 1, 32, 2)
+    G = to_dev(torch, np.ones((n, P), np.float32))
+    ticks = np.array([5, 1, np.iinfo(np.int64).max, 3, np.iinfo(np.int64).max, 2], np.int64)
+    for k in (0, n + 1):
+        with pytest.raises(pb.DBWError) as e:
+            ctx.aggregate_fastest(G, to_dev(torch, ticks), k)
+        assert e.value.status == pb.DBW_ERANGE
+    g, mask = ctx.aggregate_fastest(G, to_dev(torch, ticks), 4)       # 4 workers arrive
+    ctx.sync()
+    assert host(mask).tolist() == [1, 1, 0, 1, 0, 1]
+    ctx.aggregate_fastest(G, to_dev(torch, ticks), 5)                 # only 4 ever arrive
+    with pytest.raises(pb.DBWError) as e:
+        ctx.sync()
+    assert e.value.status == pb.DBW_ERANGE
+
+
+# -- statistics ----------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,P,k", [(4, 7840, 2), (16, 7840, 16), (64, 30720, 40), (7, 1001, 3), (40, 4096, 39)])
+def test_grad_stats(n, P, k):
+    rng = np.random.default_rng(n + P + k)
+    G = (rng.standard_normal((n, P)) * 0.3 + 0.05).astype(np.float32)
+    loss = rng.uniform(1.0, 3.0, size=n).astype(np.float32)
+    mask = np.zeros(n, np.uint8)
+    sel = sorted(rng.choice(n, size=k, replace=False).tolist())
+    mask[sel] = 1
+    g = ops.aggregate(G, sel).astype(np.float32)
+    ctx = _ctx_for_P(n, P)
+    assert ctx.P == P
+    sq, st = ctx.grad_stats(to_dev(torch, G), to_dev(torch, mask), k, to_dev(torch, g), to_dev(torch, loss))
+    ctx.sync()
+    ref = ops.grad_stats(G, sel, g.astype(np.float64), loss)
+    st = host(st)
+    assert rel_err(host(sq), ref["sqnorm"]) <= RTOL
+    assert scalar_rel(st[0], ref["gnorm2"]) <= RTOL
+    assert scalar_rel(st[1], ref["V_plus"]) <= RTOL
+    assert abs(st[2] - ref["N_plus"]) <= RTOL * max(ref["gnorm2"], ref["V_plus"] / k)
+    assert scalar_rel(st[3], ref["F_hat"]) <= RTOL
+
+
+def test_grad_stats_k1_uses_window_and_checks_mask():
+    n, P = 5, 64
+    ctx = _ctx(n, 1, 32, 2)
+    hV = [2.0, 4.0, 9.0]
+    ctx.import_state({"t": 3, "k_prev": 5, "hV": hV, "hN": [0.1, 0.2, 0.3], "hL": [1.0, 2.0], "nF": 2,
+                      "F_prev": 1.0, "F_prev2": 1.1})
+    rng = np.random.default_rng(3)
+    G = rng.standard_normal((n, P)).astype(np.float32)
+    mask = np.array([0, 0, 1, 0, 0], np.uint8)
+    loss = np.arange(1, n + 1, dtype=np.float32)
+    g = G[2].copy()
+    sq, st = ctx.grad_stats(to_dev(torch, G), to_dev(torch, mask), 1, to_dev(torch, g), to_dev(torch, loss))
+    ctx.sync()
+    st = host(st)
+    assert st[1] == pytest.approx(np.mean(hV), rel=1e-15)
+    assert st[3] == pytest.approx(3.0, rel=1e-7)
+    ctx.grad_stats(to_dev(torch, G), to_dev(torch, mask), 2, to_dev(torch, g), to_dev(torch, loss))
+    with pytest.raises(pb.DBWError):
+        ctx.sync()
+
+
+# -- choice of k ------------------------------------------------------------------------
+
+def _state(t, k_prev, hV, hN, hL, F):
+    return {"t": t, "k_prev": k_prev, "hV": hV, "hN": hN, "hL": hL, "nF": min(len(F), 2),
+            "F_prev": F[-1] if F else 0.0, "F_prev2": F[-2] if len(F) >= 2 else 0.0}
+
+
+def _random_state(rng, n, D):
+    t = int(rng.integers(0, 20))
+    nV = min(t, D)
+    hV = rng.uniform(0.0, 3.0, size=nV).tolist()
+    hN = rng.uniform(0.0, 1.0, size=nV).tolist()
+    hL = rng.normal(0.0, 20.0, size=min(max(t - 1, 0), D)).tolist()
+    F = rng.uniform(1.0, 2.0, size=min(t, 2)).tolist()
+    k_prev = int(rng.integers(1, n + 1)) if t > 0 else n
+    return t, k_prev, hV, hN, hL, F
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 7, 16, 64, 255, 256, 300])
+def test_choose_b_matches_oracle_random_states(n):
+    rng = np.random.default_rng(51 + n)
+    D = 5
+    ctx = _ctx(n, 1, 4, 2, D=D)
+    for trial in range(30):
+        t, k_prev, hV, hN, hL, F = _random_state(rng, n, D)
+        T = np.sort(rng.uniform(1.0, 5.0, size=n)) * 2 ** 20
+        if trial % 7 == 0:
+            T[rng.integers(0, n)] = np.nan           # an ineligible k
+        ctx.import_state(_state(t, k_prev, hV, hN, hL, F))
+        k, b, obj = ctx.choose_b(to_dev(torch, T))
+        ctx.sync()
+        T_list = [None if np.isnan(x) else float(x) for x in T]
+        k_ref, obj_ref = odbw.choose_k(n, 0.1, 1.01, D, hV, hN, hL, F, k_prev, T_list)
+        kg = int(host(k)[0])
+        assert k_acceptable(obj_ref, kg, k_ref), (trial, kg, k_ref)
+        assert int(host(b)[0]) == n - kg
+        og = host(obj)
+        if obj_ref is None:
+            assert np.all(np.isnan(og))
+        else:
+            for i, v in enumerate(obj_ref):
+                if v is None:
+                    assert np.isnan(og[i])
+                else:
+                    assert og[i] == pytest.approx(v, rel=1e-13, abs=1e-300)
+
+
+def test_choose_b_guard_and_negative_gains():
+    n = 8
+    ctx = _ctx(n, 1, 4, 2)
+    T = to_dev(torch, np.arange(1, n + 1, dtype=np.float64) * 1e6)
+    # L < 0: the ratio is largest at k = 1 unless the loss guard fires
+    ctx.import_state(_state(5, 3, [3.0] * 5, [0.1] * 5, [-5.0] * 4, [1.0, 1.0]))
+    k, _, _ = ctx.choose_b(T)
+    ctx.sync()
+    assert int(host(k)[0]) == 1
+    ctx.import_state(_state(5, 3, [3.0] * 5, [0.1] * 5, [-5.0] * 4, [1.0, 1.03]))
+    k, _, _ = ctx.choose_b(T)
+    ctx.sync()
+    assert int(host(k)[0]) == 4
+    # every gain negative -> wait for all n
+    ctx.import_state(_state(5, 3, [3.0] * 5, [0.0] * 5, [5.0] * 4, [1.0, 1.0]))
+    k, b, _ = ctx.choose_b(T)
+    ctx.sync()
+    assert int(host(k)[0]) == n and int(host(b)[0]) == 0

@@ -1,0 +1,193 @@
+"""GPU parity of a full DBW iteration (dbw_step) against the oracle.
+
+Lockstep: before every iteration the oracle's state (parameters rounded to
+fp32, estimator windows, arrival-time samples, clock) is imported into the
+GPU context, one dbw_step runs, and every output is compared: the time
+estimate, the objective and k (ties within 1e-6 relative accepted), the mask
+(bit-exact), worker gradients and losses, the mean gradient, the statistics,
+the parameter update, the smoothness estimate pushed into the state, and the
+arrival-time grid and clock (exact).  Free-running: the GPU runs alone and
+its k sequence is compared with the oracle's up to the first near-tie."""
+import numpy as np
+import pytest
+
+from dbw_inputs import C1, C2, C3, C5, SOFTMAX, DBWConfig, TimeModel, gather, init_params
+from dbw_inputs import generate as gen
+from oracle import dbw as odbw
+from gpu_util import RTOL, host, k_acceptable, rel_err, scalar_rel, to_dev
+
+torch = pytest.importorskip("torch")
+pb = pytest.importorskip("paper_2004_14696_amd")
+
+pytestmark = pytest.mark.gpu
+
+EPS32 = float(np.finfo(np.float32).eps)
+
+TINY = DBWConfig(name="tiny", model=SOFTMAX, n=6, B=16, d=40, C=4, S=500, iters=40, features="uniform",
+                 labels="teacher", times=TimeModel(kind="shifted_exp", shift=0.5, rate=1.0), seed=4242)
+
+
+def _setup(cfg):
+    X, y = gen.dataset(cfg)
+    ctx = pb.Context(pb.config_from(cfg, S=cfg.S))
+    return X, y, ctx, to_dev(torch, X), to_dev(torch, y)
+
+
+def _compare_iteration(cfg, rec, out, k_gpu, w_prev32, w_new, st_before, st_after, tag):
+    n = cfg.n
+    T_ref = rec["T_hat"]
+    T_gpu = host(out["T_hat"])
+    for kk in range(n):
+        if T_ref[kk] is None:
+            assert np.isnan(T_gpu[kk]), (tag, kk)
+        else:
+            assert T_gpu[kk] == pytest.approx(T_ref[kk], rel=1e-12), (tag, kk)
+    assert k_acceptable(rec["objective"], k_gpu, rec["k"]), (tag, k_gpu, rec["k"])
+    obj = host(out["objective"])
+    if rec["objective"] is not None:
+        for kk, v in enumerate(rec["objective"]):
+            if v is not None:
+                assert obj[kk] == pytest.approx(v, rel=1e-9, abs=1e-300), (tag, kk)
+    assert rel_err(host(out["G"]), rec["G"]) <= RTOL, tag
+    assert rel_err(host(out["loss"]), rec["loss"]) <= RTOL, tag
+    if k_gpu != rec["k"]:
+        return False           # a tie picked another k: the rest differs legitimately
+    assert np.array_equal(host(out["mask"]), rec["mask"]), tag
+    assert rel_err(host(out["g"]), rec["g"]) <= RTOL, tag
+    s = host(out["stats"])
+    k = rec["k"]
+    assert scalar_rel(s[0], rec["gnorm2"]) <= RTOL, tag
+    assert scalar_rel(s[1], rec["V_plus"]) <= RTOL, tag
+    assert abs(s[2] - rec["N_plus"]) <= RTOL * max(rec["gnorm2"], rec["V_plus"] / k), tag
+    assert scalar_rel(s[3], rec["F_hat"]) <= RTOL, tag
+    sq = host(out["sqnorm"])
+    ref_sq = np.zeros(n)
+    for j in rec["sel"]:
+        ref_sq[j] = float(rec["G"][j] @ rec["G"][j])
+    assert rel_err(sq, ref_sq) <= RTOL, tag
+    # parameter update: w_{t+1} - w_t = -eta g_t
+    dw = w_new.astype(np.float64) - w_prev32.astype(np.float64)
+    ref_dw = -cfg.eta * rec["g"]
+    assert np.max(np.abs(dw - ref_dw)) <= RTOL * np.max(np.abs(ref_dw)) + 2 * EPS32 * np.max(np.abs(w_prev32)), tag
+    # estimator state pushed by the GPU, from the GPU's own statistics
+    assert st_after["t"] == st_before["t"] + 1 and st_after["k_prev"] == k, tag
+    assert st_after["hV"][-1] == pytest.approx(s[1], rel=1e-15), tag
+    assert st_after["hN"][-1] == pytest.approx(s[2], rel=1e-15, abs=1e-300), tag
+    assert st_after["F_prev"] == pytest.approx(s[3], rel=1e-15), tag
+    if rec["L_plus"] is None:
+        assert st_after["hL"] == st_before["hL"], tag
+    else:
+        L_from_gpu_stats = odbw.l_estimate(cfg.eta, st_before["hN"][-1], st_before["hV"][-1], st_before["k_prev"],
+                                           st_before["F_prev"], float(s[3]))
+        assert st_after["hL"][:-1] == (st_before["hL"] + [None])[-cfg.D:][:-1], tag
+        assert st_after["hL"][-1] == pytest.approx(L_from_gpu_stats, rel=1e-12), tag
+    return True
+
+
+def _lockstep(cfg, iters):
+    X, y, ctx, Xd, yd = _setup(cfg)
+    orc = odbw.DBWOracle(cfg, init_params(cfg))
+    ties = 0
+    for t in range(iters):
+        idx = gen.batch_indices(cfg, t)
+        ticks = gen.round_trip_ticks(cfg, t)
+        w32 = orc.w.astype(np.float32)
+        orc.w = w32.astype(np.float64)
+        st = orc.export_state()
+        ctx.import_state(st)
+        ctx.import_samples(np.array(st["cnt"], np.int64), np.array(st["tsum"], np.int64), st["clock"])
+        st_before = ctx.export_state()
+        wd = to_dev(torch, w32)
+        k_gpu = ctx.step(wd, Xd, yd, ticks, rows=to_dev(torch, idx), wait=True)
+        out = ctx.step_outputs()
+        ctx.sync()
+        st_after = ctx.export_state()
+        cnt_g, tsum_g, clock_g = ctx.export_samples()
+        Xt, yt = gather(X, y, idx)
+        rec = orc.step(Xt, yt, ticks)
+        same = _compare_iteration(cfg, rec, out, k_gpu, w32, host(wd), st_before, st_after, (cfg.name, t))
+        ties += not same
+        if same:
+            assert np.array_equal(cnt_g, np.array(orc.cnt, np.int64)), (cfg.name, t)
+            assert np.array_equal(tsum_g, np.array(orc.tsum, np.int64)), (cfg.name, t)
+            assert clock_g == orc.clock, (cfg.name, t)
+    assert ties <= max(1, iters // 20), f"{ties} near-tie choices in {iters} iterations"
+    return orc
+
+
+def test_lockstep_tiny_teacher():
+    orc = _lockstep(TINY, TINY.iters)
+    assert len(set(orc.ks)) > 1    # the teacher labels make k move
+
+
+def test_lockstep_4_workers_full_run():
+    _lockstep(C1, C1.iters)
+
+
+def test_lockstep_16_workers_full_run():
+    _lockstep(C2, C2.iters)
+
+
+def test_lockstep_64_workers_first_iterations():
+    _lockstep(C3, 12)
+
+
+def test_lockstep_256_workers_100_classes_first_iterations():
+    _lockstep(C5, 3)
+
+
+@pytest.mark.parametrize("cfg", [TINY, C1], ids=lambda c: c.name)
+def test_free_running_trajectory(cfg):
+    X, y, ctx, Xd, yd = _setup(cfg)
+    orc = odbw.DBWOracle(cfg, init_params(cfg))
+    wd = to_dev(torch, init_params(cfg))
+    for t in range(cfg.iters):
+        idx = gen.batch_indices(cfg, t)
+        ticks = gen.round_trip_ticks(cfg, t)
+        k_gpu = ctx.step(wd, Xd, yd, ticks, rows=to_dev(torch, idx), wait=True)
+        Xt, yt = gather(X, y, idx)
+        rec = orc.step(Xt, yt, ticks)
+        if k_gpu != rec["k"]:
+            assert k_acceptable(rec["objective"], k_gpu, rec["k"], tol=1e-4), (t, k_gpu, rec["k"])
+            return          # trajectories legitimately part after a near-tie
+        out = ctx.step_outputs()
+        assert scalar_rel(host(out["stats"])[3], rec["F_hat"]) <= 1e-3, t
+    assert rel_err(host(wd), orc.w) <= 1e-3
+
+
+def test_step_is_bitwise_deterministic():
+    cfg = C2
+    X, y = gen.dataset(cfg)
+    res = []
+    for _ in range(2):
+        ctx = pb.Context(pb.config_from(cfg, S=cfg.S))
+        Xd, yd = to_dev(torch, X), to_dev(torch, y)
+        wd = to_dev(torch, init_params(cfg))
+        ks = [ctx.step(wd, Xd, yd, gen.round_trip_ticks(cfg, t), rows=to_dev(torch, gen.batch_indices(cfg, t)),
+                       wait=True) for t in range(6)]
+        out = ctx.step_outputs()
+        res.append((ks, host(wd), {k: host(v) for k, v in out.items()}))
+    assert res[0][0] == res[1][0]
+    assert np.array_equal(res[0][1], res[1][1])
+    for name in res[0][2]:
+        assert np.array_equal(res[0][2][name], res[1][2][name], equal_nan=True), name
+
+
+def test_materialised_and_gathered_steps_agree():
+    cfg = C1
+    X, y = gen.dataset(cfg)
+    ws = []
+    for gathered in (True, False):
+        ctx = pb.Context(pb.config_from(cfg, S=cfg.S if gathered else 0))
+        wd = to_dev(torch, init_params(cfg))
+        Xd, yd = (to_dev(torch, X), to_dev(torch, y)) if gathered else (None, None)
+        for t in range(5):
+            idx = gen.batch_indices(cfg, t)
+            if gathered:
+                ctx.step(wd, Xd, yd, gen.round_trip_ticks(cfg, t), rows=to_dev(torch, idx))
+            else:
+                Xt, yt = gather(X, y, idx)
+                ctx.step(wd, to_dev(torch, Xt), to_dev(torch, yt), gen.round_trip_ticks(cfg, t))
+        ctx.sync()
+        ws.append(host(wd))
+    assert np.array_equal(ws[0], ws[1])
