@@ -1,0 +1,188 @@
+"""Benchmark of the DBW hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C3] [--no-cpu-baseline]
+
+One step = one full DBW iteration (dbw_step): host time estimate, choice of
+k, all n worker minibatch gradients, fastest-k aggregation, statistics, SGD
+update and estimator bookkeeping.  Inputs are resident in HBM before the timed
+region: the synthetic dataset, the per-iteration minibatch row indices and the
+parameters; the per-iteration round-trip ticks are host arrays, as the
+interface defines them.  Prints one JSON line.
+
+Default workload: softmax regression with 64 workers x 256 rows, 3072
+features (32x32x3-shaped) and 10 classes -- the bandwidth-bound workload the
+metric's %-of-peak-HBM figure refers to.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "worker-gradient samples/sec per DBW iteration (1 MI355X); % peak HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+
+
+def grads_bytes(cfg, P: int, gathered: bool) -> int:
+    """Algorithmic bytes of one worker-gradient launch: every minibatch row
+    and label read once, row indices, the parameters, and the n gradient rows
+    and losses written."""
+    rows = cfg.n * cfg.B
+    return 4 * (rows * cfg.d + rows + (rows if gathered else 0) + P + cfg.n * P + cfg.n)
+
+
+def step_bytes(cfg, P: int, k: int, gathered: bool) -> int:
+    """Algorithmic bytes of one iteration: gradient launch, the k received
+    gradient rows read once, parameters read and written, mean gradient
+    written."""
+    return grads_bytes(cfg, P, gathered) + 4 * (k * P + 3 * P)
+
+
+def cpu_baseline(cfg, iters_cap: int, budget_s: float):
+    """The oracle timed on this host on the first iterations of the same
+    workload (bounded sample)."""
+    from dbw_inputs import gather, init_params
+    from dbw_inputs import generate as gen
+    from oracle import dbw as odbw
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    X, y = gen.dataset(cfg)
+    orc = odbw.DBWOracle(cfg, init_params(cfg))
+    done, spent = 0, 0.0
+    while done < iters_cap and spent < budget_s:
+        idx = gen.batch_indices(cfg, done)
+        Xt, yt = gather(X, y, idx)
+        ticks = gen.round_trip_ticks(cfg, done)
+        t0 = time.perf_counter()
+        orc.step(Xt, yt, ticks)
+        spent += time.perf_counter() - t0
+        done += 1
+    return {"value": cfg.n * cfg.B * done / spent, "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"first {done} iterations of the same workload, float64 numpy oracle "
+                      f"(minibatch gather untimed), {spent:.1f} s"}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="C3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the DBW hot path here simulates all n workers on a single "
+              f"MI355X; --gpus {args.gpus} is not supported.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2004_14696_amd as dbw
+    from dbw_inputs import get, init_params
+    from dbw_inputs import generate as gen
+
+    cfg = get(args.workload)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    X, y = gen.dataset(cfg)
+    Xd = torch.from_numpy(np.ascontiguousarray(X)).to(dev)
+    yd = torch.from_numpy(np.ascontiguousarray(y)).to(dev)
+    total = args.warmup + args.steps
+    rows = [torch.from_numpy(gen.batch_indices(cfg, t)).to(dev) for t in range(total)]
+    ticks = [gen.round_trip_ticks(cfg, t) for t in range(total)]
+    w = torch.from_numpy(init_params(cfg)).to(dev)
+    ctx = dbw.Context(dbw.config_from(cfg, S=cfg.S))
+    P = ctx.P
+
+    ks = []
+    for t in range(args.warmup):
+        ks.append(ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False))
+    ctx.sync()
+    ctx.profile(True)
+    ctx.profile_reset()
+    stream = ctx.stream
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for t in range(args.warmup, total):
+        ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ctx.sync()
+    gpu_ms = ev0.elapsed_time(ev1)
+    grads_ms, grads_n = ctx.kernel_time(dbw.binding.DBW_KT_GRADS)
+    agg_ms, agg_n = ctx.kernel_time(dbw.binding.DBW_KT_AGGREGATE)
+    ctx.profile(False)
+    st = ctx.export_state()
+    k_last = st["k_prev"]
+
+    ms_per_step = wall * 1e3 / args.steps     # whole job: host estimate, launches, device work
+    value = cfg.n * cfg.B / (ms_per_step / 1e3)
+    gb = grads_bytes(cfg, P, True)
+    grads_avg_s = grads_ms / grads_n / 1e3
+    achieved = gb / grads_avg_s / 1e9
+    sb = step_bytes(cfg, P, k_last, True)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: softmax regression, n={cfg.n} workers x B={cfg.B} rows, d={cfg.d}, "
+                        f"C={cfg.C}, minibatches gathered by index from a resident {cfg.S}x{cfg.d} dataset"
+            if cfg.model == "softmax" else
+            f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows",
+            "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P,
+        },
+        "roofline": {
+            "kernel": "worker gradients (dbw_worker_grads)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "bytes_per_launch": gb,
+            "avg_launch_ms": grads_avg_s * 1e3,
+            "launches": grads_n,
+        },
+        "step": {
+            "gpu_ms_per_step": gpu_ms / args.steps,
+            "wall_ms_per_step": wall * 1e3 / args.steps,
+            "bytes_per_step": sb,
+            "hbm_frac": sb / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "aggregate_ms_per_step": agg_ms / max(agg_n, 1),
+            "k_last": k_last,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, iters_cap=50, budget_s=args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

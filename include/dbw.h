@@ -195,6 +195,18 @@ dbw_status dbw_step_outputs(dbw_ctx* ctx, dbw_step_buffers* out);
  * sums, or a sum on a cell with zero count. */
 dbw_status dbw_time_estimate(int32_t n, const int64_t* cnt, const int64_t* tsum, double* T_hat);
 
+/* The same estimate kept across calls (pure host computation).  A caller that
+ * re-estimates after adding a few samples per call (one iteration's arrivals)
+ * gets the exact result of dbw_time_estimate at a fraction of the cost: the
+ * previous solution is re-certified against the new samples and only the
+ * parts that stop being optimal are re-solved.  dbw_step uses one of these
+ * inside every context.  Same arguments and errors as dbw_time_estimate. */
+typedef struct dbw_time_estimator dbw_time_estimator;
+dbw_status dbw_time_estimator_create(dbw_time_estimator** out);
+void dbw_time_estimator_destroy(dbw_time_estimator* est);
+dbw_status dbw_time_estimator_solve(dbw_time_estimator* est, int32_t n, const int64_t* cnt,
+                                    const int64_t* tsum, double* T_hat);
+
 /* Estimator state transfer (resume, lockstep testing).  HOST structs; both
  * calls synchronise the context's stream. */
 dbw_status dbw_state_export(dbw_ctx* ctx, dbw_estimator_state* out);

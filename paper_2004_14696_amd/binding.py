@@ -30,7 +30,8 @@ EXPORTED = (
     "dbw_worker_grads", "dbw_aggregate_fastest", "dbw_grad_stats", "dbw_choose_b", "dbw_step",
     "dbw_step_outputs", "dbw_time_estimate", "dbw_state_export", "dbw_state_import",
     "dbw_samples_export", "dbw_samples_import", "dbw_profile_enable", "dbw_kernel_time",
-    "dbw_profile_reset",
+    "dbw_profile_reset", "dbw_time_estimator_create", "dbw_time_estimator_destroy",
+    "dbw_time_estimator_solve",
 )
 
 
@@ -99,6 +100,12 @@ def load_library(path: str = LIB_PATH):
     lib.dbw_step_outputs.restype = st
     lib.dbw_time_estimate.argtypes = [c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_double)]
     lib.dbw_time_estimate.restype = st
+    lib.dbw_time_estimator_create.argtypes = [POINTER(P)]
+    lib.dbw_time_estimator_create.restype = st
+    lib.dbw_time_estimator_destroy.argtypes = [P]
+    lib.dbw_time_estimator_destroy.restype = None
+    lib.dbw_time_estimator_solve.argtypes = [P, c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_double)]
+    lib.dbw_time_estimator_solve.restype = st
     lib.dbw_state_export.argtypes = [P, POINTER(EstimatorState)]
     lib.dbw_state_export.restype = st
     lib.dbw_state_import.argtypes = [P, POINTER(EstimatorState)]
@@ -144,6 +151,37 @@ def time_estimate(cnt, tsum) -> np.ndarray:
     if s != DBW_OK:
         raise DBWError(s, "dbw_time_estimate rejected its input")
     return out
+
+
+class TimeEstimator:
+    """Incremental exact time estimate (dbw_time_estimator_*)."""
+
+    def __init__(self):
+        self.lib = load_library()
+        h = c_void_p()
+        s = self.lib.dbw_time_estimator_create(ctypes.byref(h))
+        if s != DBW_OK:
+            raise DBWError(s, "dbw_time_estimator_create failed")
+        self.h = h
+
+    def solve(self, cnt, tsum) -> np.ndarray:
+        cnt = np.ascontiguousarray(cnt, dtype=np.int64)
+        tsum = np.ascontiguousarray(tsum, dtype=np.int64)
+        n = cnt.shape[0]
+        if cnt.shape != (n, n) or tsum.shape != (n, n):
+            raise ValueError("cnt and tsum must be n x n")
+        out = np.empty(n, dtype=np.float64)
+        s = self.lib.dbw_time_estimator_solve(self.h, n, cnt.ctypes.data_as(POINTER(c_int64)),
+                                              tsum.ctypes.data_as(POINTER(c_int64)),
+                                              out.ctypes.data_as(POINTER(c_double)))
+        if s != DBW_OK:
+            raise DBWError(s, "dbw_time_estimator_solve rejected its input")
+        return out
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            self.lib.dbw_time_estimator_destroy(self.h)
+            self.h = None
 
 
 # ---------------------------------------------------------------------------

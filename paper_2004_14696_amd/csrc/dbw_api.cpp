@@ -92,6 +92,7 @@ struct dbw_ctx {
   std::vector<int64_t> cnt, tsum;
   int64_t clock = 0;
   std::vector<double> T_scratch;
+  dbw::IsoSolver solver;
 
   bool profiling = false;
   ProfileGroup prof[DBW_KT_COUNT];
@@ -486,7 +487,7 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   // 2. time estimate T_hat_t on the host
   std::string why;
   double* hT = c->h_T + (size_t)slot * n;
-  if (dbw::time_estimate(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
+  if (c->solver.solve(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
     return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
   int64_t* hk = c->h_ticks + (size_t)slot * n;
   std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
@@ -543,6 +544,25 @@ DBW_API dbw_status dbw_time_estimate(int32_t n, const int64_t* cnt, const int64_
   return dbw::time_estimate(n, cnt, tsum, T_hat, &why) == 0 ? DBW_OK : DBW_EINVAL;
 }
 
+struct dbw_time_estimator {
+  dbw::IsoSolver solver;
+};
+
+DBW_API dbw_status dbw_time_estimator_create(dbw_time_estimator** out) {
+  if (!out) return DBW_EINVAL;
+  *out = new (std::nothrow) dbw_time_estimator();
+  return *out ? DBW_OK : DBW_EINVAL;
+}
+
+DBW_API void dbw_time_estimator_destroy(dbw_time_estimator* est) { delete est; }
+
+DBW_API dbw_status dbw_time_estimator_solve(dbw_time_estimator* est, int32_t n, const int64_t* cnt,
+                                            const int64_t* tsum, double* T_hat) {
+  if (!est || !cnt || !tsum || !T_hat) return DBW_EINVAL;
+  std::string why;
+  return est->solver.solve(n, cnt, tsum, T_hat, &why) == 0 ? DBW_OK : DBW_EINVAL;
+}
+
 DBW_API dbw_status dbw_state_export(dbw_ctx* c, dbw_estimator_state* out) {
   if (!c || !out) return DBW_EINVAL;
   DeviceGuard dg(c->device);
@@ -592,6 +612,7 @@ DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int6
   std::memcpy(c->cnt.data(), cnt, sizeof(int64_t) * c->cnt.size());
   std::memcpy(c->tsum.data(), tsum, sizeof(int64_t) * c->tsum.size());
   c->clock = clock;
+  c->solver.reset();
   return DBW_OK;
 }
 

@@ -143,7 +143,25 @@ hipError_t launch_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel, i
                               hipStream_t s);
 
 // ---------------------------------------------------------------------------
-// Host time estimator (exact constrained least squares).
+// Host time estimator (exact constrained least squares).  An IsoSolver keeps
+// the previous solution and re-certifies it against new samples (exact warm
+// start); time_estimate() is the stateless full solve.
+class IsoSolver {
+ public:
+  IsoSolver();
+  ~IsoSolver();
+  IsoSolver(const IsoSolver&) = delete;
+  IsoSolver& operator=(const IsoSolver&) = delete;
+  // Returns 0 on success, -1 on invalid input (reason in *why).
+  int solve(int n, const int64_t* cnt, const int64_t* tsum, double* T_hat, std::string* why);
+  void reset();
+  int64_t full_solves() const;
+  int64_t warm_solves() const;
+
+ private:
+  struct Impl;
+  Impl* p_;
+};
 int time_estimate(int n, const int64_t* cnt, const int64_t* tsum, double* T_hat, std::string* why);
 
 }  // namespace dbw

@@ -102,7 +102,7 @@ def test_worker_grads_rejects_bad_rows_and_labels():
     assert e.value.status == pb.DBW_ERANGE
     ctx.sync()                                  # the flag is cleared
     yb = y.copy()
-    yb[3] = C                                   # label outside [0, C)
+    yb[idx[0, 0]] = C                           # label outside [0, C) on a used row
     ctx.worker_grads(to_dev(torch, W), to_dev(torch, X), to_dev(torch, yb), rows=to_dev(torch, idx))
     with pytest.raises(pb.DBWError):
         ctx.sync()

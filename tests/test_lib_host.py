@@ -5,6 +5,7 @@ import json
 import math
 import os
 import re
+import zlib
 from fractions import Fraction
 
 import numpy as np
@@ -112,3 +113,57 @@ def test_time_estimate_empty_and_invalid(lib):
         pb.time_estimate(np.zeros((2, 2), np.int64), np.array([[5, 0], [0, 0]]))   # sum on empty cell
     with pytest.raises(pb.DBWError):
         pb.time_estimate(np.zeros((2, 2), np.int64) + 1, np.full((2, 2), 2 ** 53, np.int64))
+
+
+def _trajectory_rows(rng, n, iters, pattern):
+    ks = [n]
+    for _ in range(iters - 1):
+        if pattern == "uniform":
+            ks.append(int(rng.integers(1, n + 1)))
+        elif pattern == "walk":
+            ks.append(int(np.clip(ks[-1] + rng.integers(-3, 4), 1, n)))
+        else:  # mostly the extremes, with guard-like increments
+            r = rng.random()
+            ks.append(1 if r < 0.4 else n if r < 0.8 else min(n, ks[-1] + 1))
+    return ks
+
+
+@pytest.mark.parametrize("n,iters,pattern,law", [
+    (5, 80, "uniform", "exp"), (16, 120, "walk", "pareto"), (16, 120, "extremes", "exp"),
+    (64, 60, "walk", "pareto"), (64, 60, "extremes", "exp"), (64, 40, "uniform", "exp"),
+    (256, 25, "extremes", "exp"), (256, 20, "walk", "pareto")])
+def test_incremental_estimator_matches_oracle_along_trajectories(lib, n, iters, pattern, law):
+    # Samples of iteration t land in row k_{t-1}; the incremental solver sees
+    # the grid after every iteration and must equal the exact oracle each time.
+    rng = np.random.default_rng(zlib.crc32(repr((n, iters, pattern, law)).encode()))
+    est = pb.TimeEstimator()
+    cnt = np.zeros((n, n), np.int64)
+    tsum = np.zeros((n, n), np.int64)
+    ks = _trajectory_rows(rng, n, iters, pattern)
+    for t in range(iters):
+        h = ks[t - 1] if t > 0 else n
+        tau = (1 + rng.exponential(2.0, size=n)) if law == "exp" else (1 - rng.random(n)) ** (-1 / 2.5)
+        cnt[h - 1] += 1
+        tsum[h - 1] += np.sort(np.rint(tau * 2 ** 20).astype(np.int64))
+        got = est.solve(cnt, tsum)
+        if n <= 64 or t % 4 == 0 or t == iters - 1:
+            ref = te.time_estimate(cnt.tolist(), tsum.tolist())
+            for k in range(n):
+                if ref[k] is None:
+                    assert math.isnan(got[k])
+                else:
+                    assert got[k] == pytest.approx(ref[k], rel=1e-14, abs=0), (t, k)
+        else:
+            np.testing.assert_array_equal(got, pb.time_estimate(cnt, tsum))
+
+
+def test_incremental_estimator_handles_arbitrary_changes(lib):
+    # Grids that change arbitrarily between calls (rows appear and vanish,
+    # partial rows) still give the stateless solver's exact result.
+    rng = np.random.default_rng(44)
+    est = pb.TimeEstimator()
+    for _ in range(200):
+        n = int(rng.integers(1, 9))
+        rows = sorted(set(int(x) for x in rng.integers(1, n + 1, size=int(rng.integers(1, 4)))))
+        cnt, tsum = _grid(rng, n, rows, int(rng.integers(1, 5)), full=bool(rng.random() < 0.5), law="small")
+        np.testing.assert_array_equal(est.solve(cnt, tsum), pb.time_estimate(cnt, tsum))
