@@ -103,7 +103,10 @@ int64_t dbw_param_count(const dbw_config* cfg);
  * default stream) on the current device.  Validates cfg (n in [1, DBW_MAX_N],
  * B, d, C >= 1, C <= 4096, H >= 1 for the MLP, D in [1, DBW_MAX_D], eta > 0,
  * beta >= 1, S >= 0), allocates all device workspace (no allocation happens in
- * later calls) and sets the estimator state to its initial value. */
+ * later calls) and sets the estimator state to its initial value.  Returns
+ * DBW_EUNSUPPORTED when one array the kernels address (P floats, the n*B*d
+ * minibatch floats, the S*d dataset floats, n*B*C or n*B*H activations)
+ * would reach 2 GiB. */
 dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out);
 void dbw_destroy(dbw_ctx* ctx);
 const char* dbw_last_error(const dbw_ctx* ctx);

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "dbw.h"
+#include "dbw_buffer.h"
 #include "dbw_internal.h"
 
 #define DBW_API extern "C" __attribute__((visibility("default")))
@@ -65,7 +66,6 @@ struct dbw_ctx {
   int32_t* err = nullptr;
   float* Gp = nullptr;
   float* lossp = nullptr;
-  uint32_t* counters = nullptr;
   float* Z = nullptr;
   float* ce = nullptr;
   float* sqpart = nullptr;
@@ -235,7 +235,7 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.W = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
     a.n = cf.n; a.B = cf.B; a.d = cf.d; a.C = cf.C;
     a.G = G; a.loss = loss;
-    a.Gp = c->Gp; a.lossp = c->lossp; a.counters = c->counters; a.Z = c->Z; a.ce = c->ce;
+    a.Gp = c->Gp; a.lossp = c->lossp; a.Z = c->Z; a.ce = c->ce;
     a.err = c->err;
     e = dbw::launch_softmax_grads(c->splan, a, c->stream);
   } else {
@@ -272,6 +272,16 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   *out = nullptr;
   std::string why;
   if (!config_ok(cfg, &why)) return DBW_EINVAL;
+  {
+    // every array a kernel addresses through one buffer resource must stay
+    // below 2 GiB
+    const int64_t P = param_count(*cfg);
+    const int64_t lim = dbw::kMaxBufferBytes;
+    if (P * 4 > lim || (int64_t)cfg->n * cfg->B * cfg->d * 4 > lim || cfg->S * cfg->d * 4 > lim ||
+        (int64_t)cfg->n * cfg->B * cfg->C * 4 > lim ||
+        (cfg->model == DBW_MLP && (int64_t)cfg->n * cfg->B * cfg->H * 4 > lim))
+      return DBW_EUNSUPPORTED;
+  }
   dbw_ctx* c = new (std::nothrow) dbw_ctx();
   if (!c) return DBW_EINVAL;
   c->cfg = *cfg;
@@ -302,14 +312,13 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
        sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
        sSt = take(sizeof(dbw_estimator_state)), sErr = take(4),
        sSqp = take(sizeof(float) * n * c->agg_nblocks), sPart = take(sizeof(double) * 2 * c->agg_nblocks);
-  Span sGp, sLp, sCnt, sZ, sCe, sA, sH, sdA, sR;
+  Span sGp, sLp, sZ, sCe, sA, sH, sdA, sR;
   if (cf.model == DBW_SOFTMAX) {
     if (c->splan.fused) {
       if (c->splan.slabs > 1) {
         sGp = take(sizeof(float) * n * c->splan.slabs * P);
         sLp = take(sizeof(float) * n * c->splan.slabs);
       }
-      sCnt = take(sizeof(uint32_t) * n);
     } else {
       sZ = take(sizeof(float) * rowsN * cf.C);
       sCe = take(sizeof(float) * rowsN);
@@ -331,7 +340,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   c->objective = (double*)at(sObj); c->k = (int32_t*)at(sK); c->b = (int32_t*)at(sB);
   c->sel = (int32_t*)at(sSel); c->ticks = (int64_t*)at(sTicks); c->st = (dbw_estimator_state*)at(sSt);
   c->err = (int32_t*)at(sErr); c->sqpart = (float*)at(sSqp); c->part = (double*)at(sPart);
-  c->Gp = (float*)at(sGp); c->lossp = (float*)at(sLp); c->counters = (uint32_t*)at(sCnt);
+  c->Gp = (float*)at(sGp); c->lossp = (float*)at(sLp);
   c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->A = (float*)at(sA); c->Hh = (float*)at(sH);
   c->dA = (float*)at(sdA); c->R = (float*)at(sR);
 

@@ -54,7 +54,6 @@ struct SoftmaxArgs {
   // workspace
   float* Gp;             // [n*slabs][d*C] slab partials (fused, slabs > 1)
   float* lossp;          // [n*slabs]
-  uint32_t* counters;    // [n], zero between launches
   float* Z;              // [n*B][C] logits / residuals (GEMM path)
   float* ce;             // [n*B] per-row CE (GEMM path)
   int32_t* err;

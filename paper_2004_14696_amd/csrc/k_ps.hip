@@ -19,6 +19,7 @@
 #include <cmath>
 #include <cstdint>
 
+#include "dbw_buffer.h"
 #include "dbw_internal.h"
 
 namespace dbw {
@@ -169,20 +170,14 @@ __global__ __launch_bounds__(256) void k_mask_to_sel(const uint8_t* mask, int n,
 template <bool VEC4>
 __device__ __forceinline__ void load_tile(const float* __restrict__ row, int64_t base, int lane,
                                           int64_t P, float v[4]) {
+  // columns >= P fall outside the row's resource and read as 0
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(row, static_cast<uint32_t>(P * 4));
   if (VEC4) {
-    const int64_t c = base + lane * 4;
-    if (c < P) {
-      const float4 q = *reinterpret_cast<const float4*>(row + c);
-      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-    } else {
-      v[0] = v[1] = v[2] = v[3] = 0.f;
-    }
+    const float4 q = buf_f32x4(r, static_cast<uint32_t>((base + lane * 4) * 4));
+    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
   } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t c = base + lane + WAVE * q;
-      v[q] = c < P ? row[c] : 0.f;
-    }
+    for (int q = 0; q < 4; ++q) v[q] = buf_f32(r, static_cast<uint32_t>((base + lane + WAVE * q) * 4));
   }
 }
 
@@ -208,11 +203,11 @@ __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
   // shift: the mean itself (given) or the fastest worker's row
   float c[4];
   if (MODE == AGG_STATS_GIVEN_MEAN) load_tile<VEC4>(a.g_in, base, lane, P, c);
-  else load_tile<VEC4>(a.G + (int64_t)a.sel[0] * P, base, lane, P, c);
+  else load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(a.sel[0]) * P, base, lane, P, c);
 
   float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
   for (int r = wv; r < k; r += AGG_WAVES) {
-    const int j = a.sel[r];
+    const int j = __builtin_amdgcn_readfirstlane(a.sel[r]);   // uniform per wave
     float x[4];
     load_tile<VEC4>(a.G + (int64_t)j * P, base, lane, P, x);
     float sq = 0.f;

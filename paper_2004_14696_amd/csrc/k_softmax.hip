@@ -12,8 +12,8 @@
 //    chunks of R: per-thread partial logits are reduced across the block
 //    through LDS, R threads run the softmax, and every thread folds the
 //    residuals into its accumulator.  A worker's rows are split over
-//    `slabs` blocks (to fill the 256 CUs); slab partials are combined in a
-//    fixed order by the last block of the worker to finish.
+//    `slabs` blocks (to fill the 256 CUs); a second kernel sums the slab
+//    partials in a fixed order.
 //  * GEMM path -- any C: logits Z = X W (tiled fp32 GEMM), row softmax in
 //    place (residuals), then a per-worker GEMM G_i = X_i^T R_i.
 //
@@ -24,6 +24,7 @@
 #include <cmath>
 #include <cstdint>
 
+#include "dbw_buffer.h"
 #include "dbw_internal.h"
 
 namespace dbw {
@@ -61,6 +62,8 @@ __device__ __forceinline__ int64_t xcd_logical(int64_t b, int64_t per_xcd) {
   return (b % NXCD) * per_xcd + b / NXCD;
 }
 
+constexpr int FUSED_MAX_ROWS = 1024;   // rows of one slab staged in LDS
+
 template <int CP, int M, int T, int R>
 __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, int rps, int64_t per_xcd) {
   constexpr int V = R * CP;            // partial logits per thread
@@ -71,7 +74,8 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
   __shared__ float red2[G][V];
   __shared__ float rr[V];
   __shared__ float sh_loss[R];
-  __shared__ int sh_last;
+  __shared__ int sh_row[FUSED_MAX_ROWS];
+  __shared__ int sh_lab[FUSED_MAX_ROWS];
 
   const int64_t logical = xcd_logical(blockIdx.x, per_xcd);
   if (logical >= (int64_t)a.n * slabs) return;
@@ -80,55 +84,66 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
   const int tid = threadIdx.x;
   const int d = a.d, C = a.C;
   const int64_t P = (int64_t)d * C;
+  const int b0 = q * rps;
+  const int b1 = min(a.B, b0 + rps);
+  const int nrows = b1 - b0;
 
+  // the slab's row indices and labels, validated once
+  for (int r = tid; r < nrows; r += T) {
+    const int64_t row = sample_row(a, i, b0 + r, true);
+    sh_row[r] = static_cast<int>(row);
+    sh_lab[r] = sample_label(a, row, true);
+  }
+
+  // this thread's slice of W; features j >= d and classes c >= C read as 0
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(a.W, static_cast<uint32_t>(P * 4));
   float wr[M][CP];
   float acc[M][CP];
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     const int j = tid + m * T;
-    const int jc = min(j, d - 1);
 #pragma unroll
     for (int c = 0; c < CP; ++c) {
-      const float v = a.W[(int64_t)jc * C + min(c, C - 1)];
-      wr[m][c] = (j < d && c < C) ? v : 0.f;
+      const uint32_t off = c < C ? static_cast<uint32_t>((j * C + c) * 4) : kOutOfRange;
+      wr[m][c] = buf_f32(wrs, off);
       acc[m][c] = 0.f;
     }
   }
   float loss_acc = 0.f;
   const float invB = 1.0f / static_cast<float>(a.B);
-  const int b0 = q * rps;
-  const int b1 = min(a.B, b0 + rps);
+  __syncthreads();
 
-  for (int bb = b0; bb < b1; bb += R) {
-    // issue the chunk's loads first (clamped addresses, no branches)
-    float x[R][M];
+  // rows of chunk `cb` (relative to b0) into x; rows past the slab read as 0
+  auto load_chunk = [&](int cb, float (&x)[R][M]) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      const int b = bb + r;
-      const bool row_ok = b < b1;
-      // the row is the same for the whole block: keep its address scalar
-      const int64_t row = sample_row(a, i, row_ok ? b : b0, tid == 0);
-      const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(row));
-      const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(row >> 32));
-      const float* xp = a.X + ((static_cast<int64_t>(hi) << 32) | lo) * d;
+      const int rr_ = cb + r;
+      const bool row_ok = rr_ < nrows;
+      const int row = __builtin_amdgcn_readfirstlane(sh_row[row_ok ? rr_ : 0]);
+      // a resource over the row (empty past the slab): j >= d reads 0
+      const __amdgpu_buffer_rsrc_t xr =
+          make_rsrc(a.X + static_cast<int64_t>(row) * d, row_ok ? static_cast<uint32_t>(d * 4) : 0u);
 #pragma unroll
-      for (int m = 0; m < M; ++m) {
-        const int j = tid + m * T;
-        const float v = xp[min(j, d - 1)];
-        x[r][m] = (row_ok && j < d) ? v : 0.f;
-      }
+      for (int m = 0; m < M; ++m) x[r][m] = buf_f32(xr, static_cast<uint32_t>((tid + m * T) * 4));
     }
-    // partial logits over this thread's slice of the features, row by row
+  };
+
+  float xa[R][M], xb[R][M];
+  load_chunk(0, xa);
+  for (int cb = 0; cb < nrows; cb += R) {
+    // partial logits over this thread's slice of the features
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
       for (int c = 0; c < CP; ++c) {
         float z = 0.f;
 #pragma unroll
-        for (int m = 0; m < M; ++m) z = fmaf(x[r][m], wr[m][c], z);
+        for (int m = 0; m < M; ++m) z = fmaf(xa[r][m], wr[m][c], z);
         red[tid][r * CP + c] = z;
       }
     }
+    // next chunk's loads fly during the reduction and the softmax
+    load_chunk(cb + R, xb);
     __syncthreads();
     if (tid < V * G) {
       const int v = tid % V, g = tid / V;
@@ -142,7 +157,7 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
     // softmax; lane (r, c) holds logit c of row r.
     if (tid < WAVE) {
       const int r = tid / 16, c = tid % 16;
-      const int b = bb + r;
+      const int rb = cb + r;
       float z = 0.f;
       if (c < CP) {
 #pragma unroll
@@ -157,8 +172,8 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
       float se = e;
 #pragma unroll
       for (int o = 8; o > 0; o >>= 1) se += __shfl_xor(se, o, 16);
-      const bool row_ok = b < b1;
-      const int lab = row_ok ? sample_label(a, sample_row(a, i, b, false), c == 0) : 0;
+      const bool row_ok = rb < nrows;
+      const int lab = row_ok ? sh_lab[rb] : 0;
       const float zy = __shfl(sh, r * 16 + lab, WAVE);
       if (c < CP) rr[r * CP + c] = row_ok ? (e / se - (c == lab ? 1.f : 0.f)) * invB : 0.f;
       // CE = log(sum_c e^{z_c - zmax}) - (z_y - zmax)
@@ -174,8 +189,12 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int c = 0; c < CP; ++c) acc[m][c] = fmaf(x[r][m], rv[c], acc[m][c]);
+        for (int c = 0; c < CP; ++c) acc[m][c] = fmaf(xa[r][m], rv[c], acc[m][c]);
     }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < M; ++m) xa[r][m] = xb[r][m];
   }
   if (tid < WAVE && tid % 16 == 0) sh_loss[tid / 16] = loss_acc;
   __syncthreads();
@@ -205,25 +224,43 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
         if (c < C) gp[(int64_t)j * C + c] = acc[m][c];
   }
   if (tid == 0) a.lossp[(int64_t)i * slabs + q] = block_loss;
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) sh_last = (atomicAdd(&a.counters[i], 1u) == static_cast<unsigned>(slabs - 1));
-  __syncthreads();
-  if (!sh_last) return;
-  __threadfence();
-  // last slab of worker i: combine the partials in slab order (coalesced)
-  const float* gpi = a.Gp + (int64_t)i * slabs * P;
-  float* gi = a.G + (int64_t)i * P;
-  for (int64_t e = tid; e < P; e += T) {
-    float s = 0.f;
-    for (int qq = 0; qq < slabs; ++qq) s += gpi[(int64_t)qq * P + e];
-    gi[e] = s;
+}
+
+// Sum of the slab partials of every worker in slab order (a kernel of its
+// own: the launch boundary orders the partial writes before these reads).
+// blockIdx.y = worker; each thread adds 4 consecutive elements.
+__global__ __launch_bounds__(256) void k_slab_reduce(SoftmaxArgs a, int slabs) {
+  const int i = blockIdx.y;
+  const int64_t P = (int64_t)a.d * a.C;
+  const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  const float* src = a.Gp + (int64_t)i * slabs * P;
+  float* dst = a.G + (int64_t)i * P;
+  if (e0 < P) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, static_cast<uint32_t>(slabs * P * 4));
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    if ((P & 3) == 0) {
+      for (int q = 0; q < slabs; ++q) {
+        const float4 v = buf_f32x4(rs, static_cast<uint32_t>((q * P + e0) * 4));
+        s0 += v.x; s1 += v.y; s2 += v.z; s3 += v.w;
+      }
+      *reinterpret_cast<float4*>(dst + e0) = make_float4(s0, s1, s2, s3);
+    } else {
+      float acc4[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int q = 0; q < slabs; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t idx = e0 + e;
+          acc4[e] += buf_f32(rs, idx < P ? static_cast<uint32_t>((q * P + idx) * 4) : kOutOfRange);
+        }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e0 + e < P) dst[e0 + e] = acc4[e];
+    }
   }
-  if (tid == 0) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     float s = 0.f;
-    for (int qq = 0; qq < slabs; ++qq) s += a.lossp[(int64_t)i * slabs + qq];
-    a.loss[i] = s * invB;
-    a.counters[i] = 0u;
+    for (int q = 0; q < slabs; ++q) s += a.lossp[(int64_t)i * slabs + q];
+    a.loss[i] = s / static_cast<float>(a.B);
   }
 }
 
@@ -242,13 +279,16 @@ __global__ __launch_bounds__(256) void k_logits_gemm(SoftmaxArgs a) {
   const int64_t m0 = (int64_t)blockIdx.y * GBM;
   const int n0 = blockIdx.x * GBN;
   const int d = a.d, C = a.C;
-  // A loader: row m0 + tid/4, k offset (tid%4)*4
+  // A loader: row m0 + tid/4, k offset (tid%4)*4; out-of-range reads are 0
   const int la_m = tid / 4, la_k = (tid % 4) * 4;
   const int64_t am = m0 + la_m;
-  const float* arow = nullptr;
+  const int64_t xrows = a.rows ? a.S : Mrows;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t ws = make_rsrc(a.W, static_cast<uint32_t>((int64_t)d * C * 4));
+  int64_t arow = -1;
   if (am < Mrows) {
     const int wi = static_cast<int>(am / a.B), wb = static_cast<int>(am % a.B);
-    arow = a.X + sample_row(a, wi, wb, la_k == 0) * d;
+    arow = sample_row(a, wi, wb, la_k == 0);
   }
   const int lb_k = tid / 16, lb_n = (tid % 16) * 4;
   float acc[4][4] = {};
@@ -256,12 +296,14 @@ __global__ __launch_bounds__(256) void k_logits_gemm(SoftmaxArgs a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int kk = k0 + la_k + e;
-      As[la_k + e][la_m] = (arow && kk < d) ? arow[kk] : 0.f;
+      const uint32_t off = (arow >= 0 && kk < d) ? static_cast<uint32_t>((arow * d + kk) * 4) : kOutOfRange;
+      As[la_k + e][la_m] = buf_f32(xs, off);
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int kk = k0 + lb_k, nn = n0 + lb_n + e;
-      Bs[lb_k][lb_n + e] = (kk < d && nn < C) ? a.W[(int64_t)kk * C + nn] : 0.f;
+      const uint32_t off = (kk < d && nn < C) ? static_cast<uint32_t>(((int64_t)kk * C + nn) * 4) : kOutOfRange;
+      Bs[lb_k][lb_n + e] = buf_f32(ws, off);
     }
     __syncthreads();
 #pragma unroll
@@ -327,18 +369,22 @@ __global__ __launch_bounds__(256) void k_grads_gemm(SoftmaxArgs a) {
   const int n0 = blockIdx.x * GBN;
   const int d = a.d, C = a.C, B = a.B;
   const int64_t P = (int64_t)d * C;
-  const float* Ri = a.Z + (int64_t)i * B * C;
+  const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.Z + (int64_t)i * B * C, static_cast<uint32_t>((int64_t)B * C * 4));
   const int l_k = tid / 16, l_x = (tid % 16) * 4;
   float acc[4][4] = {};
   for (int k0 = 0; k0 < B; k0 += GBK) {
     const int b = k0 + l_k;
-    const float* xr = b < B ? a.X + sample_row(a, i, b, false) * d : nullptr;
+    const int64_t xrow = b < B ? sample_row(a, i, b, false) : -1;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int j = j0 + l_x + e;
-      As[l_k][l_x + e] = (xr && j < d) ? xr[j] : 0.f;
+      const uint32_t xo = (xrow >= 0 && j < d) ? static_cast<uint32_t>((xrow * d + j) * 4) : kOutOfRange;
+      As[l_k][l_x + e] = buf_f32(xs, xo);
       const int nn = n0 + l_x + e;
-      Bs[l_k][l_x + e] = (b < B && nn < C) ? Ri[(int64_t)b * C + nn] : 0.f;
+      const uint32_t ro = (b < B && nn < C) ? static_cast<uint32_t>(((int64_t)b * C + nn) * 4) : kOutOfRange;
+      Bs[l_k][l_x + e] = buf_f32(rs, ro);
     }
     __syncthreads();
 #pragma unroll
@@ -387,6 +433,11 @@ hipError_t launch_fused_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_
   const int64_t per_xcd = (nb + NXCD - 1) / NXCD;
   hipLaunchKernelGGL((k_softmax_fused<CP, M, T, R>), dim3(static_cast<unsigned>(per_xcd * NXCD)), dim3(T), 0, s,
                      a, p.slabs, p.rows_per_slab, per_xcd);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.slabs == 1) return e;
+  const int64_t P = (int64_t)a.d * a.C;
+  const dim3 g2(static_cast<unsigned>((P + 1023) / 1024), static_cast<unsigned>(a.n));
+  hipLaunchKernelGGL(k_slab_reduce, g2, dim3(256), 0, s, a, p.slabs);
   return hipGetLastError();
 }
 
@@ -418,7 +469,8 @@ SoftmaxPlan softmax_plan(int n, int B, int d, int C) {
   int M = (d + T - 1) / T;
   if (T == 256) M = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 0;
   else M = M <= 2 ? 2 : M <= 4 ? 4 : M <= 6 ? 6 : M <= 8 ? 8 : 0;
-  if (cp == 16 && M > 6) M = 0;   // register budget (no spills up to 6)
+  // register budget: no spills for M <= 6 (C <= 10) and M <= 4 (C <= 16)
+  if ((cp == 16 && M > 4) || (cp == 10 && M > 6)) M = 0;
   if (cp == 0 || M == 0) {
     p.fused = 0;
     return p;
@@ -437,7 +489,10 @@ SoftmaxPlan softmax_plan(int n, int B, int d, int C) {
   p.rows_per_slab = (B + slabs - 1) / slabs;
   // round rows per slab up to the 4-row chunk
   p.rows_per_slab = (p.rows_per_slab + 3) / 4 * 4;
+  if (p.rows_per_slab > 1024) p.rows_per_slab = 1024;   // rows staged in LDS
   p.slabs = (B + p.rows_per_slab - 1) / p.rows_per_slab;
+  // one worker's partials are read through one buffer resource
+  if ((int64_t)p.slabs * d * C * 4 > kMaxBufferBytes) p.fused = 0;
   return p;
 }
 
