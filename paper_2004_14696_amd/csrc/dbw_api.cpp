@@ -46,6 +46,7 @@ struct dbw_ctx {
   int device = 0;
   std::string last_error;
   dbw::SoftmaxPlan splan;
+  dbw::MlpPlan mplan;
   int64_t agg_nblocks = 0;
 
   char* pool = nullptr;
@@ -70,10 +71,8 @@ struct dbw_ctx {
   float* ce = nullptr;
   float* sqpart = nullptr;
   double* part = nullptr;
-  float* A = nullptr;
   float* Hh = nullptr;
   float* dA = nullptr;
-  float* R = nullptr;
 
   // pinned host staging
   double* h_T = nullptr;        // [kSlots][n]
@@ -243,8 +242,8 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.w = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
     a.n = cf.n; a.B = cf.B; a.d = cf.d; a.H = cf.H; a.C = cf.C;
     a.G = G; a.loss = loss;
-    a.A = c->A; a.Hh = c->Hh; a.dA = c->dA; a.R = c->R; a.ce = c->ce; a.err = c->err;
-    e = dbw::launch_mlp_grads(a, c->stream);
+    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err;
+    e = dbw::launch_mlp_grads(c->mplan, a, c->stream);
   }
   if (e != hipSuccess) return fail(c, DBW_EHIP, "gradient kernels: %s", hipGetErrorString(e));
   return DBW_OK;
@@ -293,7 +292,15 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   }
   const dbw_config& cf = c->cfg;
   const int64_t n = cf.n, P = c->P, rowsN = (int64_t)cf.n * cf.B;
-  if (cf.model == DBW_SOFTMAX) c->splan = dbw::softmax_plan(cf.n, cf.B, cf.d, cf.C);
+  if (cf.model == DBW_SOFTMAX) {
+    c->splan = dbw::softmax_plan(cf.n, cf.B, cf.d, cf.C);
+  } else {
+    c->mplan = dbw::mlp_plan(cf.n, cf.B, cf.d, cf.H, cf.C);
+    if (!c->mplan.ok) {
+      delete c;
+      return DBW_EUNSUPPORTED;
+    }
+  }
   c->agg_nblocks = dbw::agg_blocks(P);
 
   // workspace layout
@@ -312,7 +319,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
        sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
        sSt = take(sizeof(dbw_estimator_state)), sErr = take(4),
        sSqp = take(sizeof(float) * n * c->agg_nblocks), sPart = take(sizeof(double) * 2 * c->agg_nblocks);
-  Span sGp, sLp, sZ, sCe, sA, sH, sdA, sR;
+  Span sGp, sLp, sZ, sCe, sH, sdA;
   if (cf.model == DBW_SOFTMAX) {
     if (c->splan.fused) {
       if (c->splan.slabs > 1) {
@@ -324,11 +331,10 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
       sCe = take(sizeof(float) * rowsN);
     }
   } else {
-    sA = take(sizeof(float) * rowsN * cf.H);
     sH = take(sizeof(float) * rowsN * cf.H);
     sdA = take(sizeof(float) * rowsN * cf.H);
-    sR = take(sizeof(float) * rowsN * cf.C);
-    sCe = take(sizeof(float) * rowsN);
+    sGp = take(sizeof(float) * n * c->mplan.slabs * c->mplan.tail);
+    sLp = take(sizeof(float) * n * c->mplan.slabs);
   }
   if (hipMalloc(&c->pool, total) != hipSuccess) {
     delete c;
@@ -341,8 +347,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   c->sel = (int32_t*)at(sSel); c->ticks = (int64_t*)at(sTicks); c->st = (dbw_estimator_state*)at(sSt);
   c->err = (int32_t*)at(sErr); c->sqpart = (float*)at(sSqp); c->part = (double*)at(sPart);
   c->Gp = (float*)at(sGp); c->lossp = (float*)at(sLp);
-  c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->A = (float*)at(sA); c->Hh = (float*)at(sH);
-  c->dA = (float*)at(sdA); c->R = (float*)at(sR);
+  c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->Hh = (float*)at(sH); c->dA = (float*)at(sdA);
 
   bool ok = hipMemset(c->pool, 0, total) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_T, sizeof(double) * kSlots * n, hipHostMallocDefault) == hipSuccess;

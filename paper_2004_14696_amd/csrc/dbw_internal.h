@@ -39,6 +39,12 @@ struct SoftmaxPlan {
 
 struct MlpPlan {
   int ok = 0;
+  int cpad = 0;           // class template (>= C)
+  int threads = 0;        // head kernel threads per block
+  int per_thread = 0;     // hidden units per head thread
+  int slabs = 1;          // row slabs per worker in the head kernel
+  int rows_per_slab = 0;
+  int64_t tail = 0;       // H + H*C + C: the [b1 | W2 | b2] segment of G
 };
 
 // Softmax regression: G = per-worker gradient of the mean CE of softmax(X W).
@@ -72,14 +78,14 @@ struct MlpArgs {
   float* G;              // [n][P]
   float* loss;           // [n]
   // workspace
-  float* A;              // [n*B][H] hidden pre-activations
   float* Hh;             // [n*B][H] hidden activations
   float* dA;             // [n*B][H] gradient w.r.t. pre-activations
-  float* R;              // [n*B][C] softmax residual (P - Y)/B
-  float* ce;             // [n*B]
+  float* Gp;             // [n*slabs][H + H*C + C] head slab partials
+  float* lossp;          // [n*slabs]
   int32_t* err;
 };
-hipError_t launch_mlp_grads(const MlpArgs& a, hipStream_t s);
+MlpPlan mlp_plan(int n, int B, int d, int H, int C);
+hipError_t launch_mlp_grads(const MlpPlan& plan, const MlpArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // PS side.

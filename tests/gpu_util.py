@@ -59,3 +59,43 @@ def k_acceptable(objective, k_gpu: int, k_ref: int, tol: float = 1e-6) -> bool:
     best = max(vals)
     v = objective[k_gpu - 1]
     return v is not None and v >= best - tol * abs(best)
+
+
+def mlp_inputs(rng, n, B, d, H, C):
+    X = rng.random((n, B, d), dtype=np.float32)
+    y = rng.integers(0, C, size=(n, B), dtype=np.int32)
+    W1 = (rng.standard_normal((d, H)) * np.sqrt(2.0 / d)).astype(np.float32)
+    b1 = (0.01 * rng.standard_normal(H)).astype(np.float32)
+    W2 = (rng.standard_normal((H, C)) * np.sqrt(2.0 / H)).astype(np.float32)
+    b2 = (0.01 * rng.standard_normal(C)).astype(np.float32)
+    w = np.concatenate([W1.ravel(), b1, W2.ravel(), b2])
+    return X, y, w
+
+
+def mlp_compare_mask(A, d, H, C, frac=1e-6):
+    """Per-worker boolean masks over the P gradient entries to compare.
+
+    The ReLU decision [A > 0] is taken in fp32 on the GPU; pre-activations
+    within fp32 rounding of zero (|A| < frac * max|A|, about 50x the rounding
+    error of a 784-term fp32 dot product) may go either way, and
+    with them the hidden unit's column of dW1 and its entry of db1.  Those
+    entries are excluded; everything else is compared.  Returns (masks, count
+    of ambiguous (worker, unit) pairs)."""
+    n = A.shape[0]
+    P = d * H + H + H * C + C
+    masks = np.ones((n, P), dtype=bool)
+    amb = 0
+    tau = frac * float(np.max(np.abs(A)))
+    for i in range(n):
+        units = np.flatnonzero(np.any(np.abs(A[i]) < tau, axis=0))
+        amb += units.size
+        for u in units:
+            masks[i, u:d * H:H] = False      # dW1[:, u]
+            masks[i, d * H + u] = False      # db1[u]
+    return masks, amb
+
+
+def masked_rel_err(a, o, mask) -> float:
+    a = np.asarray(a, dtype=np.float64)[mask]
+    o = np.asarray(o, dtype=np.float64)[mask]
+    return rel_err(a, o)

@@ -11,7 +11,8 @@ from oracle import dbw as odbw
 from oracle import model as omodel
 from oracle import ps as ops
 
-from gpu_util import RTOL, host, k_acceptable, rel_err, scalar_rel, softmax_inputs, to_dev
+from gpu_util import (RTOL, host, k_acceptable, masked_rel_err, mlp_compare_mask, mlp_inputs, rel_err,
+                      scalar_rel, softmax_inputs, to_dev)
 
 torch = pytest.importorskip("torch")
 pb = pytest.importorskip("paper_2004_14696_amd.binding")
@@ -108,6 +109,52 @@ def test_worker_grads_rejects_bad_rows_and_labels():
         ctx.sync()
     with pytest.raises(ValueError):             # shape checked before any launch
         ctx.worker_grads(to_dev(torch, W[:-1]), to_dev(torch, X), to_dev(torch, y), rows=to_dev(torch, idx))
+
+
+MLP_SHAPES = [
+    # (n, B, d, H, C)
+    (32, 64, 784, 512, 10),   # 32 workers x 64 rows, 784-512-10
+    (3, 7, 50, 40, 3),
+    (2, 5, 100, 300, 10),     # hidden width not a multiple of the block
+    (5, 13, 70, 600, 10),     # two hidden units per head thread
+    (4, 9, 33, 17, 16),
+    (1, 1, 3, 5, 2),
+]
+
+
+@pytest.mark.parametrize("n,B,d,H,C", MLP_SHAPES)
+def test_worker_grads_mlp(n, B, d, H, C):
+    rng = np.random.default_rng(2000 + n + d + H)
+    X, y, w = mlp_inputs(rng, n, B, d, H, C)
+    ctx = _ctx(n, B, d, C, model="mlp", H=H)
+    assert ctx.P == w.size
+    G, loss = ctx.worker_grads(to_dev(torch, w), to_dev(torch, X), to_dev(torch, y))
+    ctx.sync()
+    Go, lo, A = omodel.mlp_worker_grads(w.astype(np.float64), X, y, H, C, return_preact=True)
+    masks, amb = mlp_compare_mask(A, d, H, C)
+    assert amb <= max(4, A.size // 100000)         # ambiguous ReLU decisions are rare
+    Gg = host(G)
+    for i in range(n):
+        assert masked_rel_err(Gg[i], Go[i], masks[i]) <= RTOL, i
+    assert rel_err(host(loss), lo) <= RTOL
+
+
+def test_worker_grads_mlp_gathered_and_unsupported_width():
+    n, B, d, H, C, S = 4, 16, 64, 128, 10, 200
+    rng = np.random.default_rng(12)
+    Xs = rng.random((S, d), dtype=np.float32)
+    ys = rng.integers(0, C, size=S, dtype=np.int32)
+    idx = rng.integers(0, S, size=(n, B), dtype=np.int32)
+    _, _, w = mlp_inputs(rng, n, B, d, H, C)
+    ctx = _ctx(n, B, d, C, model="mlp", H=H, S=S)
+    wd = to_dev(torch, w)
+    G1, l1 = ctx.worker_grads(wd, to_dev(torch, Xs), to_dev(torch, ys), rows=to_dev(torch, idx))
+    G2, l2 = ctx.worker_grads(wd, to_dev(torch, Xs[idx]), to_dev(torch, ys[idx]))
+    ctx.sync()
+    assert torch.equal(G1, G2) and torch.equal(l1, l2)
+    with pytest.raises(pb.DBWError) as e:           # 3 hidden units per head thread: no kernel
+        _ctx(2, 4, 8, 10, model="mlp", H=1100)
+    assert e.value.status == pb.DBW_EUNSUPPORTED
 
 
 # -- aggregation --------------------------------------------------------------------
