@@ -82,6 +82,8 @@ def main(argv=None) -> int:
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="skip the per-launch HIP events (the roofline fields are then omitted)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the DBW hot path here simulates all n workers on a single "
@@ -111,7 +113,7 @@ def main(argv=None) -> int:
     for t in range(args.warmup):
         ks.append(ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False))
     ctx.sync()
-    ctx.profile(True)
+    ctx.profile(not args.no_kernel_timing)
     ctx.profile_reset()
     stream = ctx.stream
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -127,6 +129,9 @@ def main(argv=None) -> int:
     gpu_ms = ev0.elapsed_time(ev1)
     grads_ms, grads_n = ctx.kernel_time(dbw.binding.DBW_KT_GRADS)
     agg_ms, agg_n = ctx.kernel_time(dbw.binding.DBW_KT_AGGREGATE)
+    choose_ms, choose_n = ctx.kernel_time(dbw.binding.DBW_KT_CHOOSE)
+    est_ms, est_n = ctx.kernel_time(dbw.binding.DBW_KT_HOST_ESTIMATE)
+    hstep_ms, hstep_n = ctx.kernel_time(dbw.binding.DBW_KT_HOST_STEP)
     ctx.profile(False)
     st = ctx.export_state()
     k_last = st["k_prev"]
@@ -134,7 +139,7 @@ def main(argv=None) -> int:
     ms_per_step = wall * 1e3 / args.steps     # whole job: host estimate, launches, device work
     value = cfg.n * cfg.B / (ms_per_step / 1e3)
     gb = grads_bytes(cfg, P, True)
-    grads_avg_s = grads_ms / grads_n / 1e3
+    grads_avg_s = grads_ms / max(grads_n, 1) / 1e3 if grads_n else float("nan")
     achieved = gb / grads_avg_s / 1e9
     sb = step_bytes(cfg, P, k_last, True)
     out = {
@@ -175,6 +180,9 @@ def main(argv=None) -> int:
             "bytes_per_step": sb,
             "hbm_frac": sb / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS,
             "aggregate_ms_per_step": agg_ms / max(agg_n, 1),
+            "choose_ms_per_step": choose_ms / max(choose_n, 1),
+            "host_estimate_ms_per_step": est_ms / max(est_n, 1),
+            "host_step_call_ms": hstep_ms / max(hstep_n, 1),
             "k_last": k_last,
         },
     }

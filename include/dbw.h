@@ -225,8 +225,16 @@ dbw_status dbw_samples_import(dbw_ctx* ctx, const int64_t* cnt, const int64_t* t
 /* Kernel timing with HIP events on the context's stream.  When enabled, every
  * launch of the listed kernel groups is bracketed by events; dbw_kernel_time
  * synchronises and returns the summed milliseconds and the launch count since
- * the last reset. */
-typedef enum { DBW_KT_GRADS = 0, DBW_KT_AGGREGATE = 1, DBW_KT_CHOOSE = 2, DBW_KT_COUNT = 3 } dbw_kernel_group;
+ * the last reset.  The two host groups report wall-clock host time (steady
+ * clock) spent in the time-estimate solve and in the whole dbw_step call. */
+typedef enum {
+  DBW_KT_GRADS = 0,
+  DBW_KT_AGGREGATE = 1,
+  DBW_KT_CHOOSE = 2,
+  DBW_KT_HOST_ESTIMATE = 3,
+  DBW_KT_HOST_STEP = 4,
+  DBW_KT_COUNT = 5
+} dbw_kernel_group;
 dbw_status dbw_profile_enable(dbw_ctx* ctx, int32_t on);
 dbw_status dbw_kernel_time(dbw_ctx* ctx, int32_t group, double* total_ms, int64_t* launches);
 dbw_status dbw_profile_reset(dbw_ctx* ctx);

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_PKG, "libdbw.so")
 DBW_OK, DBW_EINVAL, DBW_ERANGE, DBW_EHIP, DBW_ESTATE, DBW_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 DBW_SOFTMAX, DBW_MLP = 0, 1
 DBW_MAX_N, DBW_MAX_D = 1024, 64
-DBW_KT_GRADS, DBW_KT_AGGREGATE, DBW_KT_CHOOSE = 0, 1, 2
+DBW_KT_GRADS, DBW_KT_AGGREGATE, DBW_KT_CHOOSE, DBW_KT_HOST_ESTIMATE, DBW_KT_HOST_STEP = 0, 1, 2, 3, 4
 
 STATUS_NAMES = {0: "DBW_OK", -1: "DBW_EINVAL", -2: "DBW_ERANGE", -3: "DBW_EHIP",
                 -4: "DBW_ESTATE", -5: "DBW_EUNSUPPORTED"}

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -74,10 +75,13 @@ struct dbw_ctx {
   float* Hh = nullptr;
   float* dA = nullptr;
 
-  // pinned host staging
+  // pinned host staging (coherent; kernels read and write it in place)
   double* h_T = nullptr;        // [kSlots][n]
   int64_t* h_ticks = nullptr;   // [kSlots][n]
   int32_t* h_k = nullptr;       // [kSlots]
+  double* d_T = nullptr;        // device-side addresses of the three above
+  int64_t* d_ticks = nullptr;
+  int32_t* d_k = nullptr;
   int32_t* h_err = nullptr;     // [1]
   hipEvent_t ev[kSlots]{};
 
@@ -205,6 +209,19 @@ dbw_status check_device_ptrs(dbw_ctx* c, std::initializer_list<std::pair<const v
     if (!p.first) return fail(c, DBW_EINVAL, "%s is NULL", p.second);
   return DBW_OK;
 }
+
+struct HostScope {
+  dbw_ctx* c;
+  int g;
+  std::chrono::steady_clock::time_point t0;
+  HostScope(dbw_ctx* ctx, int group) : c(ctx), g(group), t0(std::chrono::steady_clock::now()) {}
+  ~HostScope() {
+    if (!c->profiling) return;
+    ProfileGroup& pg = c->prof[g];
+    pg.done_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    pg.done_launches += 1;
+  }
+};
 
 struct ProfScope {
   dbw_ctx* c;
@@ -350,9 +367,13 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->Hh = (float*)at(sH); c->dA = (float*)at(sdA);
 
   bool ok = hipMemset(c->pool, 0, total) == hipSuccess;
-  ok = ok && hipHostMalloc((void**)&c->h_T, sizeof(double) * kSlots * n, hipHostMallocDefault) == hipSuccess;
-  ok = ok && hipHostMalloc((void**)&c->h_ticks, sizeof(int64_t) * kSlots * n, hipHostMallocDefault) == hipSuccess;
-  ok = ok && hipHostMalloc((void**)&c->h_k, sizeof(int32_t) * kSlots, hipHostMallocDefault) == hipSuccess;
+  const unsigned pin = hipHostMallocMapped | hipHostMallocCoherent;
+  ok = ok && hipHostMalloc((void**)&c->h_T, sizeof(double) * kSlots * n, pin) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_ticks, sizeof(int64_t) * kSlots * n, pin) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_k, sizeof(int32_t) * kSlots, pin) == hipSuccess;
+  ok = ok && hipHostGetDevicePointer((void**)&c->d_T, c->h_T, 0) == hipSuccess;
+  ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
+  ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
   for (int s = 0; s < kSlots && ok; ++s) ok = hipEventCreateWithFlags(&c->ev[s], hipEventDisableTiming) == hipSuccess;
   if (!ok) {
@@ -433,7 +454,7 @@ DBW_API dbw_status dbw_aggregate_fastest(dbw_ctx* c, const float* G, const int64
   DeviceGuard dg(c->device);
   ProfScope ps(c, DBW_KT_AGGREGATE);
   dbw::ChooseArgs ca{};
-  ca.ticks = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
+  ca.ticks_src = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
   ca.sel = c->sel; ca.mask = mask; ca.err = c->err;
   HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
   dbw::AggArgs aa{};
@@ -474,7 +495,7 @@ DBW_API dbw_status dbw_choose_b(dbw_ctx* c, const double* T_hat, int32_t* k_out,
   DeviceGuard dg(c->device);
   ProfScope ps(c, DBW_KT_CHOOSE);
   dbw::ChooseArgs ca{};
-  ca.st = c->st; ca.T_hat = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
+  ca.st = c->st; ca.T_src = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
   ca.do_choose = 1; ca.do_select = 0; ca.k_out = k_out; ca.b_out = b_out; ca.objective = objective;
   ca.err = c->err;
   HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
@@ -491,6 +512,7 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   for (int i = 0; i < n; ++i)
     if (ticks_host[i] < 0) return fail(c, DBW_EINVAL, "tick of worker %d is negative", i);
   DeviceGuard dg(c->device);
+  HostScope hs_step(c, DBW_KT_HOST_STEP);
   const int64_t t = c->t;
   const int slot = static_cast<int>(t % kSlots);
   // 1. arrival times of iterations up to t-1 into the grid (needs k_{t-2}),
@@ -501,20 +523,24 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   // 2. time estimate T_hat_t on the host
   std::string why;
   double* hT = c->h_T + (size_t)slot * n;
-  if (c->solver.solve(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
-    return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  {
+    HostScope hs(c, DBW_KT_HOST_ESTIMATE);
+    if (c->solver.solve(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
+      return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  }
   int64_t* hk = c->h_ticks + (size_t)slot * n;
   std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
   std::vector<int64_t>& srt = c->sorted[slot];
   srt.assign(ticks_host, ticks_host + n);
   std::sort(srt.begin(), srt.end());
-  HIP_TRY(c, hipMemcpyAsync(c->T_hat, hT, sizeof(double) * n, hipMemcpyHostToDevice, c->stream));
-  HIP_TRY(c, hipMemcpyAsync(c->ticks, hk, sizeof(int64_t) * n, hipMemcpyHostToDevice, c->stream));
-  // 3. choose k_t and select the first k_t arrivals
+  // 3. choose k_t and select the first k_t arrivals; the kernel reads T_hat
+  //    and the ticks from the pinned slot, keeps device copies, and writes
+  //    k_t back into the pinned slot
   {
     ProfScope ps(c, DBW_KT_CHOOSE);
     dbw::ChooseArgs ca{};
-    ca.st = c->st; ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.n = n; ca.eta = c->cfg.eta;
+    ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
+    ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.k_host = c->d_k + slot; ca.n = n; ca.eta = c->cfg.eta;
     ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
     HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
@@ -534,8 +560,7 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
     HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
   }
-  // 6. k_t back to the host for the arrival-time bookkeeping
-  HIP_TRY(c, hipMemcpyAsync(c->h_k + slot, c->k, sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+  // 6. the slot's k_t is in pinned memory once this event has passed
   HIP_TRY(c, hipEventRecord(c->ev[slot], c->stream));
   c->t = t + 1;
   if (k_host) {
@@ -634,8 +659,8 @@ DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
   if (!c) return DBW_EINVAL;
   DeviceGuard dg(c->device);
   if (on) {
-    for (auto& pg : c->prof)
-      while (static_cast<int>(pg.start.size()) < kProfilePairs) {
+    for (int g = 0; g < DBW_KT_HOST_ESTIMATE; ++g)
+      for (auto& pg = c->prof[g]; static_cast<int>(pg.start.size()) < kProfilePairs;) {
         hipEvent_t a, b;
         HIP_TRY(c, hipEventCreate(&a));
         HIP_TRY(c, hipEventCreate(&b));

@@ -91,8 +91,11 @@ hipError_t launch_mlp_grads(const MlpPlan& plan, const MlpArgs& a, hipStream_t s
 // PS side.
 struct ChooseArgs {
   const dbw_estimator_state* st;  // device
-  const double* T_hat;            // device [n] (choose)
-  const int64_t* ticks;           // device [n] (select)
+  const double* T_src;            // [n] time estimates (device or pinned host)
+  const int64_t* ticks_src;       // [n] ticks (device or pinned host)
+  double* T_hat;                  // nullable device copy of T_src
+  int64_t* ticks;                 // nullable device copy of ticks_src
+  int32_t* k_host;                // nullable pinned host copy of k
   int n;
   double eta, beta;
   int do_choose, do_select;

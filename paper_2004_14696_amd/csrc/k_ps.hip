@@ -51,31 +51,73 @@ __device__ double block_sum_256(double v, double* sh /*[4]*/) {
   return r;
 }
 
+// Cooperative copy of the estimator state into LDS (whole 4-byte words).
+__device__ __forceinline__ void load_state(const dbw_estimator_state* g, dbw_estimator_state* sh) {
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(g);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(sh);
+  constexpr int W = sizeof(dbw_estimator_state) / 4;
+  for (int i = threadIdx.x; i < W; i += blockDim.x) dst[i] = src[i];
+}
+
+__device__ __forceinline__ void store_state(const dbw_estimator_state* sh, dbw_estimator_state* g) {
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(sh);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(g);
+  constexpr int W = sizeof(dbw_estimator_state) / 4;
+  for (int i = threadIdx.x; i < W; i += blockDim.x) dst[i] = src[i];
+}
+
+// (objective, k) of the better choice: larger objective, then larger k.
+__device__ __forceinline__ void better(double& r, int& k, double r2, int k2) {
+  if (k2 != 0 && (k == 0 || r2 > r || (r2 == r && k2 > k))) {
+    r = r2;
+    k = k2;
+  }
+}
+
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
 #pragma clang fp contract(off)
-  __shared__ double sh_r[256];
-  __shared__ double sh_g[256];
-  __shared__ int sh_k[256];
-  __shared__ int sh_kfinal;
+  __shared__ dbw_estimator_state st;
+  __shared__ double sh_T[DBW_MAX_N];
   __shared__ long long sh_t[DBW_MAX_N];
-  __shared__ int sh_cnt[256];
-  const int tid = threadIdx.x;
+  __shared__ double sh_r[4], sh_g[4], sh_win[3];
+  __shared__ int sh_k[4], sh_cnt[4];
+  __shared__ int sh_kfinal;
+  const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
   const int n = a.n;
 
+  // stage the inputs (T_hat and ticks may live in pinned host memory)
   if (a.do_choose) {
-    const dbw_estimator_state* st = a.st;
-    // D-window means: the state keeps only the last D entries, oldest first.
-    double V = 0.0, N = 0.0, L = 0.0;
-    for (int i = 0; i < st->nV; ++i) V += st->hV[i];
-    for (int i = 0; i < st->nV; ++i) N += st->hN[i];
-    for (int i = 0; i < st->nL; ++i) L += st->hL[i];
-    const bool hasL = st->nL > 0;
-    if (st->nV > 0) {
-      V = V / st->nV;
-      N = N / st->nV;
+    load_state(a.st, &st);
+    for (int k = tid; k < n; k += blockDim.x) {
+      const double T = a.T_src[k];
+      sh_T[k] = T;
+      if (a.T_hat) a.T_hat[k] = T;
     }
-    if (hasL) L = L / st->nL;
+  }
+  if (a.do_select) {
+    for (int i = tid; i < n; i += blockDim.x) {
+      const long long t = a.ticks_src[i];
+      sh_t[i] = t;
+      if (a.ticks) a.ticks[i] = t;
+    }
+  }
+  __syncthreads();
+
+  if (a.do_choose) {
+    // D-window means (oldest first, summed in order as the definition reads)
+    if (tid == 0) {
+      double V = 0.0, N = 0.0, L = 0.0;
+      for (int i = 0; i < st.nV; ++i) V += st.hV[i];
+      for (int i = 0; i < st.nV; ++i) N += st.hN[i];
+      for (int i = 0; i < st.nL; ++i) L += st.hL[i];
+      sh_win[0] = st.nV > 0 ? V / st.nV : 0.0;
+      sh_win[1] = st.nV > 0 ? N / st.nV : 0.0;
+      sh_win[2] = st.nL > 0 ? L / st.nL : 0.0;
+    }
+    __syncthreads();
+    const bool hasL = st.nL > 0;
+    const double V = sh_win[0], N = sh_win[1], L = sh_win[2];
     const double ga = a.eta - L * a.eta * a.eta / 2.0;
     const double gb = L * a.eta * a.eta / 2.0;
     double best_r = -INFINITY;
@@ -83,51 +125,46 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
     double maxG = -INFINITY;
     for (int k = tid + 1; k <= n; k += blockDim.x) {
       const double Gk = ga * N - gb * V / k;
-      const double T = a.T_hat[k - 1];
+      const double T = sh_T[k - 1];
       const bool eligible = isfinite(T) && T > 0.0;
       const double r = eligible ? Gk / T : NAN;
       if (a.objective) a.objective[k - 1] = hasL ? r : NAN;
       maxG = fmax(maxG, Gk);
-      if (eligible && (best_k == 0 || r > best_r || (r == best_r && k > best_k))) {
-        best_r = r;
-        best_k = k;
-      }
+      if (eligible) better(best_r, best_k, r, k);
     }
-    sh_r[tid] = best_r;
-    sh_k[tid] = best_k;
-    sh_g[tid] = maxG;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      better(best_r, best_k, __shfl_xor(best_r, o, WAVE), __shfl_xor(best_k, o, WAVE));
+      maxG = fmax(maxG, __shfl_xor(maxG, o, WAVE));
+    }
+    if (lane == 0) {
+      sh_r[wv] = best_r;
+      sh_k[wv] = best_k;
+      sh_g[wv] = maxG;
+    }
     __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (tid < s) {
-        const double r2 = sh_r[tid + s];
-        const int k2 = sh_k[tid + s];
-        if (k2 != 0 && (sh_k[tid] == 0 || r2 > sh_r[tid] || (r2 == sh_r[tid] && k2 > sh_k[tid]))) {
-          sh_r[tid] = r2;
-          sh_k[tid] = k2;
-        }
-        sh_g[tid] = fmax(sh_g[tid], sh_g[tid + s]);
-      }
-      __syncthreads();
-    }
     if (tid == 0) {
-      int k = (!hasL || sh_k[0] == 0 || sh_g[0] < 0.0) ? n : sh_k[0];
+      double r = sh_r[0], g = sh_g[0];
+      int kb = sh_k[0];
+      for (int w = 1; w < 4; ++w) {
+        better(r, kb, sh_r[w], sh_k[w]);
+        g = fmax(g, sh_g[w]);
+      }
+      int k = (!hasL || kb == 0 || g < 0.0) ? n : kb;
       // loss guard: never decrease k while the loss estimate rises
-      if (st->nF >= 2 && st->F_prev > a.beta * st->F_prev2 && st->k_prev < n)
-        k = max(k, st->k_prev + 1);
+      if (st.nF >= 2 && st.F_prev > a.beta * st.F_prev2 && st.k_prev < n) k = max(k, st.k_prev + 1);
       a.k_out[0] = k;
       a.b_out[0] = n - k;
+      if (a.k_host) *a.k_host = k;
       sh_kfinal = k;
     }
-    __syncthreads();
-  } else {
-    if (tid == 0) sh_kfinal = a.k_imm;
-    __syncthreads();
+  } else if (tid == 0) {
+    sh_kfinal = a.k_imm;
   }
+  __syncthreads();
 
   if (a.do_select) {
     const int k = sh_kfinal;
-    for (int i = tid; i < n; i += blockDim.x) sh_t[i] = a.ticks[i];
-    __syncthreads();
     int finite = 0;
     for (int i = tid; i < n; i += blockDim.x) {
       const long long ti = sh_t[i];
@@ -141,13 +178,11 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
       if (on) a.sel[rank] = i;
       finite += ti < INT64_MAX;
     }
-    sh_cnt[tid] = finite;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) finite += __shfl_xor(finite, o, WAVE);
+    if (lane == 0) sh_cnt[wv] = finite;
     __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (tid < s) sh_cnt[tid] += sh_cnt[tid + s];
-      __syncthreads();
-    }
-    if (tid == 0 && k > sh_cnt[0]) atomicOr(a.err, ERR_K_RANGE);
+    if (tid == 0 && k > sh_cnt[0] + sh_cnt[1] + sh_cnt[2] + sh_cnt[3]) atomicOr(a.err, ERR_K_RANGE);
   }
 }
 
@@ -169,9 +204,9 @@ __global__ __launch_bounds__(256) void k_mask_to_sel(const uint8_t* mask, int n,
 // loads; needs P % 4 == 0).  Otherwise lane owns columns lane + 64 q.
 template <bool VEC4>
 __device__ __forceinline__ void load_tile(const float* __restrict__ row, int64_t base, int lane,
-                                          int64_t P, float v[4]) {
-  // columns >= P fall outside the row's resource and read as 0
-  const __amdgpu_buffer_rsrc_t r = make_rsrc(row, static_cast<uint32_t>(P * 4));
+                                          int64_t P, float v[4], bool valid = true) {
+  // columns >= P (and every column of an invalid row) read as 0
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(row, valid ? static_cast<uint32_t>(P * 4) : 0u);
   if (VEC4) {
     const float4 q = buf_f32x4(r, static_cast<uint32_t>((base + lane * 4) * 4));
     v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
@@ -206,21 +241,31 @@ __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
   else load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(a.sel[0]) * P, base, lane, P, c);
 
   float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int r = wv; r < k; r += AGG_WAVES) {
-    const int j = __builtin_amdgcn_readfirstlane(a.sel[r]);   // uniform per wave
-    float x[4];
-    load_tile<VEC4>(a.G + (int64_t)j * P, base, lane, P, x);
-    float sq = 0.f;
+  constexpr int U = 4;   // rows in flight per wave
+  for (int r0 = wv; r0 < k; r0 += AGG_WAVES * U) {
+    float x[U][4];
+    int jj[U];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float dv = x[q] - c[q];
-      s1[q] += dv;
-      s2[q] = fmaf(dv, dv, s2[q]);
-      sq = fmaf(x[q], x[q], sq);
+    for (int u = 0; u < U; ++u) {
+      const int r = r0 + u * AGG_WAVES;
+      jj[u] = r < k ? __builtin_amdgcn_readfirstlane(a.sel[r]) : -1;   // uniform per wave
+      load_tile<VEC4>(a.G + (int64_t)(jj[u] < 0 ? 0 : jj[u]) * P, base, lane, P, x[u], jj[u] >= 0);
     }
-    if (MODE != AGG_MEAN) {
-      sq = wave_sum(sq);
-      if (lane == 0) a.sqpart[(int64_t)j * nblocks + blk] = sq;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (jj[u] < 0) break;
+      float sq = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float dv = x[u][q] - c[q];
+        s1[q] += dv;
+        s2[q] = fmaf(dv, dv, s2[q]);
+        sq = fmaf(x[u][q], x[u][q], sq);
+      }
+      if (MODE != AGG_MEAN) {
+        sq = wave_sum(sq);
+        if (lane == 0) a.sqpart[(int64_t)jj[u] * nblocks + blk] = sq;
+      }
     }
   }
 #pragma unroll
@@ -299,6 +344,8 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
     return;
   }
   // block 0: statistics and estimator bookkeeping
+  __shared__ dbw_estimator_state st;
+  load_state(a.st, &st);
   double m2 = 0.0, g2 = 0.0, ls = 0.0, cnt = 0.0;
   for (int64_t b = tid; b < a.nblocks; b += blockDim.x) {
     m2 += a.part[b * 2 + 0];
@@ -313,43 +360,48 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
   g2 = block_sum_256(g2, sh_red);
   ls = block_sum_256(ls, sh_red);
   cnt = block_sum_256(cnt, sh_red);
-  if (tid != 0) return;
-  if (static_cast<int>(cnt) != k) atomicOr(a.err, ERR_MASK_COUNT);
-  dbw_estimator_state* st = a.st;
-  double V_plus;
-  if (k >= 2) {
-    V_plus = m2 / (k - 1);
-  } else {
-    double s = 0.0;
-    for (int i = 0; i < st->nV; ++i) s += st->hV[i];
-    V_plus = st->nV > 0 ? s / st->nV : 0.0;
-  }
-  const double N_plus = fmax(g2 - V_plus / k, 0.0);
-  const double F_hat = ls / k;
-  a.stats->gnorm2 = g2;
-  a.stats->V_plus = V_plus;
-  a.stats->N_plus = N_plus;
-  a.stats->F_hat = F_hat;
-  if (!a.bookkeeping) return;
-  const double eta = a.eta;
-  if (st->t >= 1 && st->nV >= 1) {
-    const double Nl = st->hN[st->nV - 1], Vl = st->hV[st->nV - 1];
-    const double den = eta * eta * (Nl + Vl / st->k_prev);
-    if (den > 0.0) {
-      const double Lp = 2.0 * (eta * Nl - (st->F_prev - F_hat)) / den;
-      push_window(st->hL, &st->nL, a.D, Lp);
+  if (tid == 0) {
+    if (static_cast<int>(cnt) != k) atomicOr(a.err, ERR_MASK_COUNT);
+    double V_plus;
+    if (k >= 2) {
+      V_plus = m2 / (k - 1);
+    } else {
+      double s = 0.0;
+      for (int i = 0; i < st.nV; ++i) s += st.hV[i];
+      V_plus = st.nV > 0 ? s / st.nV : 0.0;
+    }
+    const double N_plus = fmax(g2 - V_plus / k, 0.0);
+    const double F_hat = ls / k;
+    a.stats->gnorm2 = g2;
+    a.stats->V_plus = V_plus;
+    a.stats->N_plus = N_plus;
+    a.stats->F_hat = F_hat;
+    if (a.bookkeeping) {
+      const double eta = a.eta;
+      if (st.t >= 1 && st.nV >= 1) {
+        const double Nl = st.hN[st.nV - 1], Vl = st.hV[st.nV - 1];
+        const double den = eta * eta * (Nl + Vl / st.k_prev);
+        if (den > 0.0) {
+          const double Lp = 2.0 * (eta * Nl - (st.F_prev - F_hat)) / den;
+          push_window(st.hL, &st.nL, a.D, Lp);
+        }
+      }
+      int32_t nv = st.nV;
+      push_window(st.hV, &nv, a.D, V_plus);
+      nv = st.nV;
+      push_window(st.hN, &nv, a.D, N_plus);
+      st.nV = nv;
+      st.F_prev2 = st.F_prev;
+      st.F_prev = F_hat;
+      st.nF = st.nF < 2 ? st.nF + 1 : 2;
+      st.k_prev = k;
+      st.t += 1;
     }
   }
-  int32_t nv = st->nV;
-  push_window(st->hV, &nv, a.D, V_plus);
-  nv = st->nV;
-  push_window(st->hN, &nv, a.D, N_plus);
-  st->nV = nv;
-  st->F_prev2 = st->F_prev;
-  st->F_prev = F_hat;
-  st->nF = st->nF < 2 ? st->nF + 1 : 2;
-  st->k_prev = k;
-  st->t += 1;
+  if (a.bookkeeping) {
+    __syncthreads();
+    store_state(&st, a.st);
+  }
 }
 
 }  // namespace
