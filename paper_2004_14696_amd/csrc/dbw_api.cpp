@@ -3,15 +3,19 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <condition_variable>
 #include <cstring>
 #include <initializer_list>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -83,7 +87,8 @@ struct dbw_ctx {
   int64_t* d_ticks = nullptr;
   int32_t* d_k = nullptr;
   int32_t* h_err = nullptr;     // [1]
-  hipEvent_t ev[kSlots]{};
+  hipEvent_t ev[kSlots]{};      // end of the slot's iteration (recorded on request)
+  hipEvent_t ev_k[kSlots]{};    // after the slot's choice kernel: k is in h_k
 
   // host bookkeeping of arrival times
   int64_t t = 0;                // next iteration index (== device state t once drained)
@@ -97,11 +102,26 @@ struct dbw_ctx {
   std::vector<double> T_scratch;
   dbw::IsoSolver solver;
 
+  // Estimate worker.  T_hat_{t+1} depends on k_{t-1} only, so it is solved on
+  // a host thread of its own while the GPU runs iterations t-1 and t; the
+  // launching thread then only queues kernels.  While a job is posted the
+  // worker owns the grid, the clock, the solver and the pinned T slots.
+  std::thread worker;
+  std::mutex mu;
+  std::condition_variable cv;
+  bool quit = false;
+  int64_t job_u = -1;               // iteration whose T_hat the job solves
+  std::atomic<int> job_state{0};    // 0 none, 1 posted, 2 finished
+  dbw_status job_status = DBW_OK;
+  std::string job_error;
+
   bool profiling = false;
   ProfileGroup prof[DBW_KT_COUNT];
 };
 
 namespace {
+
+thread_local bool t_in_worker = false;  // errors of a job go to job_error
 
 dbw_status fail(dbw_ctx* c, dbw_status s, const char* fmt, ...) {
   if (c) {
@@ -110,7 +130,7 @@ dbw_status fail(dbw_ctx* c, dbw_status s, const char* fmt, ...) {
     va_start(ap, fmt);
     vsnprintf(buf, sizeof buf, fmt, ap);
     va_end(ap);
-    c->last_error = buf;
+    (t_in_worker ? c->job_error : c->last_error) = buf;
   }
   return s;
 }
@@ -172,8 +192,10 @@ dbw_status known_k(dbw_ctx* c, int64_t u, int32_t* k) {
     return fail(c, DBW_ESTATE, "iteration %lld precedes the context's history", (long long)u);
   }
   const int slot = static_cast<int>(u % kSlots);
-  HIP_TRY(c, hipEventSynchronize(c->ev[slot]));
+  HIP_TRY(c, hipEventSynchronize(c->ev_k[slot]));
   *k = c->h_k[slot];
+  if (*k < 1 || *k > c->cfg.n)
+    return fail(c, DBW_ESTATE, "choice of iteration %lld did not complete (k=%d)", (long long)u, *k);
   return DBW_OK;
 }
 
@@ -204,12 +226,6 @@ dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
   return DBW_OK;
 }
 
-dbw_status check_device_ptrs(dbw_ctx* c, std::initializer_list<std::pair<const void*, const char*>> ps) {
-  for (auto& p : ps)
-    if (!p.first) return fail(c, DBW_EINVAL, "%s is NULL", p.second);
-  return DBW_OK;
-}
-
 struct HostScope {
   dbw_ctx* c;
   int g;
@@ -222,6 +238,67 @@ struct HostScope {
     pg.done_launches += 1;
   }
 };
+
+// T_hat_u into the pinned slot of iteration u: fold the arrivals of iteration
+// u-1 into row k_{u-2} and the clock through iteration u-2, then solve.  The
+// slot's previous reader, the choice kernel of iteration u-4, precedes the
+// choice of iteration u-2 that the fold waits for.
+dbw_status estimate(dbw_ctx* c, int64_t u) {
+  if (dbw_status s = fold(c, u, std::max<int64_t>(c->clocked, u - 1)); s != DBW_OK) return s;
+  HostScope hs(c, DBW_KT_HOST_ESTIMATE);
+  std::string why;
+  double* hT = c->h_T + (size_t)(u % kSlots) * c->cfg.n;
+  if (c->solver.solve(c->cfg.n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
+    return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  return DBW_OK;
+}
+
+void worker_main(dbw_ctx* c) {
+  t_in_worker = true;
+  (void)hipSetDevice(c->device);
+  std::unique_lock<std::mutex> lk(c->mu);
+  for (;;) {
+    c->cv.wait(lk, [c] { return c->quit || c->job_state.load(std::memory_order_relaxed) == 1; });
+    if (c->quit) return;
+    const int64_t u = c->job_u;
+    lk.unlock();
+    c->job_status = estimate(c, u);
+    c->job_state.store(2, std::memory_order_release);
+    lk.lock();
+  }
+}
+
+void post_estimate(dbw_ctx* c, int64_t u) {
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    c->job_u = u;
+    c->job_status = DBW_OK;
+    c->job_state.store(1, std::memory_order_relaxed);
+  }
+  c->cv.notify_one();
+}
+
+// Wait for the posted job, if any; returns its status.  The wait is short
+// (the job only waits for kernels already queued), so it spins.
+dbw_status join_estimate(dbw_ctx* c) {
+  if (c->job_state.load(std::memory_order_acquire) == 0) return DBW_OK;
+  for (int spin = 0; c->job_state.load(std::memory_order_acquire) != 2; ++spin) {
+    if (spin < 4096) __builtin_ia32_pause();
+    else std::this_thread::yield();
+  }
+  c->job_state.store(0, std::memory_order_relaxed);
+  if (c->job_status != DBW_OK) {
+    c->last_error = c->job_error;
+    return c->job_status;
+  }
+  return DBW_OK;
+}
+
+dbw_status check_device_ptrs(dbw_ctx* c, std::initializer_list<std::pair<const void*, const char*>> ps) {
+  for (auto& p : ps)
+    if (!p.first) return fail(c, DBW_EINVAL, "%s is NULL", p.second);
+  return DBW_OK;
+}
 
 struct ProfScope {
   dbw_ctx* c;
@@ -375,7 +452,10 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
-  for (int s = 0; s < kSlots && ok; ++s) ok = hipEventCreateWithFlags(&c->ev[s], hipEventDisableTiming) == hipSuccess;
+  for (int s = 0; s < kSlots && ok; ++s) {
+    ok = hipEventCreateWithFlags(&c->ev[s], hipEventDisableTiming) == hipSuccess;
+    ok = ok && hipEventCreateWithFlags(&c->ev_k[s], hipEventDisableTiming) == hipSuccess;
+  }
   if (!ok) {
     dbw_destroy(c);
     return DBW_EHIP;
@@ -394,6 +474,12 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   for (auto& v : c->sorted) v.assign(n, 0);
   c->T_scratch.assign(n, 0.0);
   reset_host_pipeline(c, 0, cf.n);
+  try {
+    c->worker = std::thread(worker_main, c);
+  } catch (...) {
+    dbw_destroy(c);
+    return DBW_EINVAL;
+  }
   *out = c;
   return DBW_OK;
 }
@@ -401,8 +487,19 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
 DBW_API void dbw_destroy(dbw_ctx* c) {
   if (!c) return;
   DeviceGuard g(c->device);
+  if (c->worker.joinable()) {
+    (void)join_estimate(c);
+    {
+      std::lock_guard<std::mutex> lk(c->mu);
+      c->quit = true;
+    }
+    c->cv.notify_one();
+    c->worker.join();
+  }
   if (c->stream || c->pool) (void)hipStreamSynchronize(c->stream);
   for (auto& ev : c->ev)
+    if (ev) (void)hipEventDestroy(ev);
+  for (auto& ev : c->ev_k)
     if (ev) (void)hipEventDestroy(ev);
   for (auto& pg : c->prof) {
     for (auto e : pg.start) (void)hipEventDestroy(e);
@@ -515,19 +612,14 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   HostScope hs_step(c, DBW_KT_HOST_STEP);
   const int64_t t = c->t;
   const int slot = static_cast<int>(t % kSlots);
-  // 1. arrival times of iterations up to t-1 into the grid (needs k_{t-2}),
-  //    clock through iteration t-2.
-  if (dbw_status s = fold(c, t, std::max<int64_t>(c->clocked, t - 1)); s != DBW_OK) return s;
-  // the slot's previous user (iteration t - kSlots) has drained: its event
-  // was waited for above (k_{t-2} is newer).
-  // 2. time estimate T_hat_t on the host
-  std::string why;
-  double* hT = c->h_T + (size_t)slot * n;
+  // 1. T_hat_t in the pinned slot: solved by the worker since k_{t-2} became
+  //    known, or here when no job was posted (first step of a history)
   {
-    HostScope hs(c, DBW_KT_HOST_ESTIMATE);
-    if (c->solver.solve(n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
-      return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+    const bool posted = c->job_state.load(std::memory_order_acquire) != 0;
+    if (dbw_status s = posted ? join_estimate(c) : estimate(c, t); s != DBW_OK) return s;
   }
+  // 2. this iteration's ticks into the pinned slot (its previous reader, the
+  //    choice of t-4, precedes the choice of t-2 the estimate waited for)
   int64_t* hk = c->h_ticks + (size_t)slot * n;
   std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
   std::vector<int64_t>& srt = c->sorted[slot];
@@ -545,6 +637,7 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
     HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
   }
+  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
   // 4. worker gradients
   if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, c->loss); s != DBW_OK) return s;
   // 5. aggregate, statistics, update, estimator bookkeeping
@@ -560,10 +653,11 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
     HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
   }
-  // 6. the slot's k_t is in pinned memory once this event has passed
-  HIP_TRY(c, hipEventRecord(c->ev[slot], c->stream));
   c->t = t + 1;
+  // 6. T_hat_{t+1} on the worker (it waits for k_{t-1})
+  post_estimate(c, t + 1);
   if (k_host) {
+    HIP_TRY(c, hipEventRecord(c->ev[slot], c->stream));
     HIP_TRY(c, hipEventSynchronize(c->ev[slot]));
     *k_host = c->h_k[slot];
   }
@@ -612,6 +706,7 @@ DBW_API dbw_status dbw_state_export(dbw_ctx* c, dbw_estimator_state* out) {
 
 DBW_API dbw_status dbw_state_import(dbw_ctx* c, const dbw_estimator_state* in) {
   if (!c || !in) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   const dbw_config& cf = c->cfg;
   if (in->t < 0 || in->k_prev < 1 || in->k_prev > cf.n || in->nV < 0 || in->nV > cf.D || in->nL < 0 ||
       in->nL > cf.D || in->nF < 0 || in->nF > 2)
@@ -629,6 +724,7 @@ DBW_API dbw_status dbw_state_import(dbw_ctx* c, const dbw_estimator_state* in) {
 
 DBW_API dbw_status dbw_samples_export(dbw_ctx* c, int64_t* cnt, int64_t* tsum, int64_t* clock) {
   if (!c || !cnt || !tsum || !clock) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
@@ -640,6 +736,7 @@ DBW_API dbw_status dbw_samples_export(dbw_ctx* c, int64_t* cnt, int64_t* tsum, i
 
 DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int64_t* tsum, int64_t clock) {
   if (!c || !cnt || !tsum) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   const int n = c->cfg.n;
   std::vector<double> probe(n);
   std::string why;
@@ -657,6 +754,7 @@ DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int6
 
 DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
   if (!c) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
   if (on) {
     for (int g = 0; g < DBW_KT_HOST_ESTIMATE; ++g)
@@ -674,6 +772,7 @@ DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
 
 DBW_API dbw_status dbw_kernel_time(dbw_ctx* c, int32_t group, double* total_ms, int64_t* launches) {
   if (!c || !total_ms || !launches || group < 0 || group >= DBW_KT_COUNT) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   ProfileGroup& pg = c->prof[group];
@@ -691,6 +790,7 @@ DBW_API dbw_status dbw_kernel_time(dbw_ctx* c, int32_t group, double* total_ms, 
 
 DBW_API dbw_status dbw_profile_reset(dbw_ctx* c) {
   if (!c) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   for (auto& pg : c->prof) {
