@@ -124,7 +124,8 @@ dbw_status dbw_sync(dbw_ctx* ctx);
  * Minibatches: if rows == NULL, X is DEVICE float [n][B][d] and y DEVICE int32
  * [n][B]; else X is the resident dataset DEVICE float [S][d], y its labels
  * DEVICE int32 [S], and rows DEVICE int32 [n][B] lists each worker's row
- * indices into it.  Labels must lie in [0, C). */
+ * indices into it.  Labels must lie in [0, C).  w, X and G must be 16-byte
+ * aligned (DBW_EINVAL otherwise). */
 dbw_status dbw_worker_grads(dbw_ctx* ctx, const float* w, const float* X, const int32_t* y,
                             const int32_t* rows, float* G, float* loss);
 
@@ -159,7 +160,7 @@ dbw_status dbw_choose_b(dbw_ctx* ctx, const double* T_hat, int32_t* k_out, int32
 /* One full DBW iteration t: estimate T_hat from the arrival times recorded so
  * far (host, Eq. quadratic_opt), choose k_t, compute all n worker gradients,
  * aggregate the k_t first arrivals, compute the statistics, update
- * w <- w - eta g_t (w DEVICE float [P], in place), and push the estimator
+ * w <- w - eta g_t (w DEVICE float [P], 16-byte aligned, in place), and push the estimator
  * state.  X, y, rows as in dbw_worker_grads.  ticks_host (HOST int64 [n]) are
  * this iteration's round-trip ticks; they are recorded as samples of row
  * h = k_{t-1} once k_{t-1} is known, and advance the virtual clock by the

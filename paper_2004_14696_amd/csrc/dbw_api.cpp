@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <condition_variable>
+#include <cstdint>
 #include <cstring>
 #include <initializer_list>
 #include <limits>
@@ -343,8 +344,11 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
   return DBW_OK;
 }
 
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 dbw_status check_batch(dbw_ctx* c, const float* X, const int32_t* y, const int32_t* rows) {
   if (!X || !y) return fail(c, DBW_EINVAL, "X and y must be non-NULL");
+  if (!aligned16(X)) return fail(c, DBW_EINVAL, "X must be 16-byte aligned");
   if (rows && c->cfg.S <= 0) return fail(c, DBW_EINVAL, "row indices need a dataset: create the context with S > 0");
   return DBW_OK;
 }
@@ -417,7 +421,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   if (cf.model == DBW_SOFTMAX) {
     if (c->splan.fused) {
       if (c->splan.slabs > 1) {
-        sGp = take(sizeof(float) * n * c->splan.slabs * P);
+        sGp = take(sizeof(float) * n * c->splan.slabs * c->splan.part);
         sLp = take(sizeof(float) * n * c->splan.slabs);
       }
     } else {
@@ -537,6 +541,7 @@ DBW_API dbw_status dbw_worker_grads(dbw_ctx* c, const float* w, const float* X, 
                                     const int32_t* rows, float* G, float* loss) {
   if (!c) return DBW_EINVAL;
   if (dbw_status s = check_device_ptrs(c, {{w, "w"}, {G, "G"}, {loss, "loss"}}); s != DBW_OK) return s;
+  if (!aligned16(w) || !aligned16(G)) return fail(c, DBW_EINVAL, "w and G must be 16-byte aligned");
   if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
   DeviceGuard g(c->device);
   return launch_grads(c, w, X, y, rows, G, loss);
@@ -603,6 +608,7 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
                             const int64_t* ticks_host, int32_t* k_host) {
   if (!c) return DBW_EINVAL;
   if (dbw_status s = check_device_ptrs(c, {{w, "w"}}); s != DBW_OK) return s;
+  if (!aligned16(w)) return fail(c, DBW_EINVAL, "w must be 16-byte aligned");
   if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
   if (!ticks_host) return fail(c, DBW_EINVAL, "ticks_host is NULL");
   const int n = c->cfg.n;

@@ -29,12 +29,13 @@ inline int64_t agg_blocks(int64_t P) { return (P + AGG_TILE - 1) / AGG_TILE; }
 // ---------------------------------------------------------------------------
 // Worker-gradient plans.
 struct SoftmaxPlan {
-  int fused = 0;          // 1: single-pass kernel (small C); 0: GEMM path
+  int fused = 0;          // 2: matrix-core single pass; 1: VALU single pass; 0: GEMM path
   int threads = 0;        // fused: threads per block
-  int per_thread = 0;     // fused: d-elements per thread (M)
+  int per_thread = 0;     // fused 1: d-elements per thread (M); fused 2: float4 groups per lane (U)
   int cpad = 0;           // fused: class template (>= C)
   int slabs = 1;          // fused: row slabs per worker
   int rows_per_slab = 0;
+  int64_t part = 0;       // floats of one slab partial (fused, slabs > 1)
 };
 
 struct MlpPlan {

@@ -23,6 +23,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "dbw_buffer.h"
 #include "dbw_internal.h"
@@ -224,6 +225,411 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
         if (c < C) gp[(int64_t)j * C + c] = acc[m][c];
   }
   if (tid == 0) a.lossp[(int64_t)i * slabs + q] = block_loss;
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core variant of the single pass (C <= 16, d % 4 == 0, d <= 3072).
+//
+// Eight waves split the feature dimension; wave w owns features
+// w*64U + 64u + 4m + j (u < U, m < 16, j < 4).  Rows stream through in
+// chunks of 8; lane (m, g) = (lane % 16, lane / 16) holds the float4
+// X[row g + 4e][w*64U + 64u + 4m .. +3] for e = 0, 1 -- exactly the A
+// operand of a 16x16x4 MFMA whose k index runs over rows and whose m index
+// runs over 16 features.  So the gradient G_i += X^T R (contraction over
+// rows) is a chain of MFMAs on the loaded registers, accumulated in 16U
+// tiles of 16 features x 16 classes.  The logits (contraction over
+// features, which sit on lane % 16) are computed on the vector ALUs: each
+// lane dots its 4U features of a row with W (staged once per block in LDS,
+// in lane order), a 16-lane DPP reduction sums the row group, and the eight
+// waves' partials meet in LDS.  Every wave then runs the softmax of the
+// chunk itself, lane (m, g) producing residual r[row g + 4e][class m] --
+// the B operand of the same MFMAs.  One block barrier per chunk.
+constexpr int MF_WAVES = 8;
+constexpr int MF_T = MF_WAVES * WAVE;
+constexpr int MF_ROWS = 8;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum / max over the 16 lanes of a DPP row; butterfly pairs (xor 1, xor 2,
+// half-mirror, mirror) leave the identical value in all 16 lanes.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x140>(v);
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return v;
+}
+
+__device__ __forceinline__ float f4_at(const float4& v, int j) {
+  return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int U, int CW>
+__global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs, int rps, int64_t per_xcd) {
+  static_assert(CW % 2 == 0 && CW <= 16, "class padding");
+  // W in lane order: lane (w, m) reads its 4U features x CW classes from one
+  // contiguous run (features w 64U + 64u + 4m + j at (4u + j) CW); the run
+  // length SL = 8a + 4 floats puts the 16 lanes of a row group on distinct
+  // bank pairs for 8-byte reads.  The same LDS later assembles the block's
+  // slice of G ([d][C]).
+  constexpr int SL = 4 * U * CW + 4;
+  constexpr int WS = MF_WAVES * 16 * SL;
+  __shared__ __attribute__((aligned(16))) float Ws[WS];
+  __shared__ float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
+  __shared__ int sh_row[FUSED_MAX_ROWS];
+  __shared__ int sh_lab[FUSED_MAX_ROWS];
+
+  const int64_t logical = xcd_logical(blockIdx.x, per_xcd);
+  if (logical >= (int64_t)a.n * slabs) return;
+  const int i = static_cast<int>(logical / slabs);
+  const int q = static_cast<int>(logical % slabs);
+  const int tid = threadIdx.x;
+  const int lane = tid & (WAVE - 1), w = tid >> 6;
+  const int m = lane & 15, g = lane >> 4;
+  const int d = a.d, C = a.C;
+  const int64_t P = (int64_t)d * C;
+  const int b0 = q * rps;
+  const int nrows = min(a.B, b0 + rps) - b0;
+
+  // W in coalesced float4 pieces (P % 4 == 0 since d % 4 == 0), issued first
+  // so that their latency overlaps the row staging
+  const int n4 = static_cast<int>(P / 4);
+  constexpr int KMAX = (MF_T * U * CW / 4 + MF_T - 1) / MF_T;   // P <= 512 U CW
+  float4 wl[KMAX];
+  {
+    const __amdgpu_buffer_rsrc_t wrs = make_rsrc(a.W, static_cast<uint32_t>(P * 4));
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const int e4 = tid + k * MF_T;
+      wl[k] = buf_f32x4(wrs, e4 < n4 ? static_cast<uint32_t>(e4 * 16) : kOutOfRange);
+    }
+  }
+  float4* w4 = reinterpret_cast<float4*>(Ws);
+  if (d < MF_T * U) {
+    // slots of features past d must read as 0 (their rows carry finite values
+    // of the same row)
+    for (int k = tid; k < WS / 4; k += MF_T) w4[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  for (int r = tid; r < nrows; r += MF_T) {
+    const int64_t row = sample_row(a, i, b0 + r, true);
+    sh_row[r] = static_cast<int>(row);
+    sh_lab[r] = sample_label(a, row, true);
+  }
+  __syncthreads();
+
+  const int64_t xrows = a.rows ? a.S : (int64_t)a.n * a.B;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const int fbase = w * 64 * U + 4 * m;
+  // byte offset of row cb + g + 4e of the slab, or kOutOfRange past the slab
+  auto row_off = [&](int cb, int e) -> uint32_t {
+    const int r = cb + g + 4 * e;
+    const int rc = r < nrows ? r : 0;
+    const int64_t row = a.rows ? (int64_t)sh_row[rc] : (int64_t)i * a.B + b0 + rc;
+    return r < nrows ? static_cast<uint32_t>(row * d * 4) : kOutOfRange;
+  };
+  // this lane's float4 of group u of a row.  A group past d reads features
+  // 0..3 of the same row instead: its W entries are 0 and its gradient rows
+  // are never stored, so only the row's own values enter (no bounds select
+  // per load; kOutOfRange + 12 KiB stays out of range).
+  auto load_u = [&](uint32_t roff, int u) -> float4 {
+    const int f = fbase + 64 * u;
+    return buf_f32x4(xr, roff + (f < d ? static_cast<uint32_t>(f * 4) : 0u));
+  };
+  float4 xa[2][U], xb[2][U];   // two chunks in flight, roles alternate
+  {
+    const uint32_t r0 = row_off(0, 0), r1 = row_off(0, 1);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      xa[0][u] = load_u(r0, u);
+      xa[1][u] = load_u(r1, u);
+    }
+  }
+
+  // Stage W.  Features 4h .. 4h+3 (group h = w' 16U + 16u + m') are 4C
+  // contiguous elements of W and 4CW contiguous floats of run (w', m') at
+  // 4u CW, so with C == CW the copy is float4 to float4.
+  {
+    // float index in Ws of element r of group h's 4CW floats
+    auto slot = [](int h, int r) { return ((h / (16 * U)) * 16 + h % 16) * SL + ((h % (16 * U)) / 16) * 4 * CW + r; };
+    if (C == CW) {
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        const int e = 4 * (tid + k * MF_T);
+        if (e < 4 * n4) w4[slot(e / (4 * CW), e % (4 * CW)) / 4] = wl[k];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        const int e4 = tid + k * MF_T;
+        if (e4 < n4) {
+          int f = (4 * e4) / C, c = 4 * e4 - f * C;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            Ws[slot(f / 4, (f % 4) * CW + c)] = f4_at(wl[k], q);
+            if (++c == C) {
+              c = 0;
+              ++f;
+            }
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  f32x4 acc[U][4];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[u][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float loss_acc = 0.f;
+  const float invB = 1.0f / static_cast<float>(a.B);
+  const bool cls_ok = m < C;
+  const int nch = (nrows + MF_ROWS - 1) / MF_ROWS;
+  float rv[2];   // residuals of the chunk whose MFMAs run next
+
+  // Partial logits of rows g, g + 4 over this lane's 4U features.  wl0 is
+  // this lane's W run.  The W reads run one feature ahead of the FMAs, and
+  // the empty asm statements pin every step in place: left alone, the
+  // compiler would hoist all 4U x CW reads to the front and hold them in
+  // registers that the row buffers need.
+  auto logits = [&](const float4 (&x)[2][U], float (&z)[2][CW], const float* wl0) {
+    float wc[CW], wn[CW];
+    auto read_w = [&](int t, float (&wv)[CW]) {
+      const float2* wp = reinterpret_cast<const float2*>(wl0 + t * CW);
+#pragma unroll
+      for (int c2 = 0; c2 < CW / 2; ++c2) {
+        const float2 v = wp[c2];
+        wv[2 * c2] = v.x;
+        wv[2 * c2 + 1] = v.y;
+      }
+    };
+    read_w(0, wc);
+#pragma unroll
+    for (int t = 0; t < 4 * U; ++t) {
+      if (t + 1 < 4 * U) read_w(t + 1, wn);
+      const float x0 = f4_at(x[0][t / 4], t % 4), x1 = f4_at(x[1][t / 4], t % 4);
+#pragma unroll
+      for (int c = 0; c < CW; ++c) {
+        z[0][c] = fmaf(x0, wc[c], z[0][c]);
+        z[1][c] = fmaf(x1, wc[c], z[1][c]);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int c = 0; c < CW; ++c) asm volatile("" : "+v"(z[e][c]));
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int c = 0; c < CW; ++c) wc[c] = wn[c];
+    }
+  };
+  // Sum the partial logits over the 16-lane row group; lane m == 0 stores
+  // the wave's partials for the block (zb[buf]).
+  auto reduce_logits = [&](float (&z)[2][CW], int buf) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) z[e][c] += dpp<0xB1>(z[e][c]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) z[e][c] += dpp<0x4E>(z[e][c]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) z[e][c] += dpp<0x141>(z[e][c]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) z[e][c] += dpp<0x140>(z[e][c]);
+    if (m == 0) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        float2* zp = reinterpret_cast<float2*>(&zb[buf][w][g + 4 * e][0]);
+#pragma unroll
+        for (int c2 = 0; c2 < CW / 2; ++c2) zp[c2] = make_float2(z[e][2 * c2], z[e][2 * c2 + 1]);
+      }
+    }
+  };
+  // After the barrier: the softmax of chunk cb's rows g, g + 4 (lane m =
+  // class) from the eight waves' partials; residuals into rv, cross entropy
+  // into the label's lane.
+  auto softmax = [&](int cb, int buf) {
+    float zt[2], mx[2], ex[2], se[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      zt[e] = 0.f;
+#pragma unroll
+      for (int v = 0; v < MF_WAVES; ++v) zt[e] += zb[buf][v][g + 4 * e][m];
+      mx[e] = cls_ok ? zt[e] : -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0xB1>(mx[e]));
+#pragma unroll
+    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x4E>(mx[e]));
+#pragma unroll
+    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x141>(mx[e]));
+#pragma unroll
+    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x140>(mx[e]));
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      ex[e] = cls_ok ? __expf(zt[e] - mx[e]) : 0.f;
+      se[e] = ex[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) se[e] += dpp<0xB1>(se[e]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) se[e] += dpp<0x4E>(se[e]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) se[e] += dpp<0x141>(se[e]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) se[e] += dpp<0x140>(se[e]);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int r = cb + g + 4 * e;
+      const bool row_ok = r < nrows;
+      const int lab = sh_lab[row_ok ? r : 0];
+      const bool hit = row_ok && m == lab;
+      // se >= 1 (the largest class contributes exp(0))
+      const float p = ex[e] * __builtin_amdgcn_rcpf(se[e]);
+      rv[e] = row_ok && cls_ok ? (p - (hit ? 1.f : 0.f)) * invB : 0.f;
+      // CE = log(sum_c e^{z_c - zmax}) - (z_y - zmax), in the label's lane
+      loss_acc += hit ? __logf(se[e]) - (zt[e] - mx[e]) : 0.f;
+    }
+  };
+  // One chunk: logits of chunk cb (rows in A) while chunk cb + 8 streams
+  // into B, the block-wide softmax, then G += X^T R on the matrix cores.
+  auto step = [&](float4 (&A)[2][U], float4 (&B)[2][U], int cb) {
+    float z[2][CW];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) z[e][c] = 0.f;
+    {
+      const uint32_t rn = row_off(cb + MF_ROWS, 0);
+#pragma unroll
+      for (int u = 0; u < U; ++u) B[0][u] = load_u(rn, u);
+    }
+    logits(A, z, &Ws[(w * 16 + m) * SL]);
+    const int buf = (cb / MF_ROWS) & 1;
+    reduce_logits(z, buf);
+    {
+      // rows g + 4 of the next chunk once the logit registers are released
+      const uint32_t rn = row_off(cb + MF_ROWS, 1);
+#pragma unroll
+      for (int u = 0; u < U; ++u) B[1][u] = load_u(rn, u);
+    }
+    __syncthreads();
+    softmax(cb, buf);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[u][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(f4_at(A[e][u], j), rv[e], acc[u][j], 0, 0, 0);
+  };
+  int c = 0;
+  for (; c + 1 < nch; c += 2) {
+    step(xa, xb, c * MF_ROWS);
+    step(xb, xa, (c + 1) * MF_ROWS);
+  }
+  if (c < nch) step(xa, xb, c * MF_ROWS);
+
+  // lane (m, g) holds tile rows 4g + t (features w 64U + 64u + 16g + 4t + j)
+  // of class m.
+  if (slabs > 1) {
+    // slab partial in tile order: float4 (t = 0..3) of (w, u, j, g, m) at
+    // ((((w U + u) 4 + j) 4 + g) C + m) 4; k_slab_reduce_tiles sums the slabs
+    // and restores the [d][C] order
+    if (cls_ok) {
+      float4* part = reinterpret_cast<float4*>(a.Gp + ((int64_t)i * slabs + q) * (int64_t)(MF_T * U * C));
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          part[(((w * U + u) * 4 + j) * 4 + g) * C + m] = make_float4(acc[u][j][0], acc[u][j][1], acc[u][j][2], acc[u][j][3]);
+    }
+  } else {
+    // the worker's G ([d][C], P contiguous floats) is assembled in the LDS
+    // that held W and written out in float4 pieces
+    __syncthreads();
+    if (cls_ok) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int f = w * 64 * U + 64 * u + 16 * g + 4 * t + j;
+            if (f < d) Ws[f * C + m] = acc[u][j][t];
+          }
+    }
+    __syncthreads();
+    const float4* s4 = reinterpret_cast<const float4*>(Ws);
+    float4* o4 = reinterpret_cast<float4*>(a.G + (int64_t)i * P);
+    for (int k = tid; k < static_cast<int>(P / 4); k += MF_T) o4[k] = s4[k];
+  }
+  if (w == 0) {
+    // the loss of a row sits in its label's lane of its row group
+    float l = loss_acc;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
+    if (lane == 0) {
+      if (slabs == 1) a.loss[i] = l * invB;
+      else a.lossp[(int64_t)i * slabs + q] = l;
+    }
+  }
+}
+
+// Sum of the tile-order slab partials of the matrix-core kernel, in slab
+// order.  Block (x, i): features 64x .. 64x + 63 of worker i, whose 64C
+// partial floats of one slab are contiguous (wave w' = x / U, group
+// u = x % U).  Summed float4 pieces are put back in [d][C] order through LDS.
+__global__ __launch_bounds__(256) void k_slab_reduce_tiles(SoftmaxArgs a, int slabs, int U) {
+  __shared__ __attribute__((aligned(16))) float tile[64 * 16];
+  const int i = blockIdx.y, x = blockIdx.x;
+  const int C = a.C, d = a.d;
+  const int64_t P = (int64_t)d * C;
+  const int64_t part = (int64_t)MF_T * U * C;
+  const int n4 = 16 * C;   // float4 pieces of the 64 features
+  for (int k = threadIdx.x; k < n4; k += 256) {
+    // piece k = ((j 4 + g) C + m): features 16g + 4t + j (t = 0..3), class m
+    const int m = k % C, jg = k / C, g = jg % 4, j = jg / 4;
+    const float* src = a.Gp + (int64_t)i * slabs * part + (int64_t)x * 64 * C + 4 * k;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < slabs; ++q) {
+      const float4 v = *reinterpret_cast<const float4*>(src + q * part);
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    tile[(16 * g + 0 + j) * C + m] = s.x;
+    tile[(16 * g + 4 + j) * C + m] = s.y;
+    tile[(16 * g + 8 + j) * C + m] = s.z;
+    tile[(16 * g + 12 + j) * C + m] = s.w;
+  }
+  __syncthreads();
+  const int f0 = x * 64;
+  const int nf = min(64, d - f0);   // features past d are not stored
+  float* dst = a.G + (int64_t)i * P + (int64_t)f0 * C;
+  for (int k = threadIdx.x; k < nf * C / 4; k += 256)
+    reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(tile)[k];
+  if (x == 0 && threadIdx.x == 0) {
+    float l = 0.f;
+    for (int q = 0; q < slabs; ++q) l += a.lossp[(int64_t)i * slabs + q];
+    a.loss[i] = l / static_cast<float>(a.B);
+  }
 }
 
 // Sum of the slab partials of every worker in slab order (a kernel of its
@@ -441,6 +847,32 @@ hipError_t launch_fused_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_
   return hipGetLastError();
 }
 
+template <int U, int CW>
+hipError_t launch_mfma_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
+  const int64_t nb = (int64_t)a.n * p.slabs;
+  const int64_t per_xcd = (nb + NXCD - 1) / NXCD;
+  hipLaunchKernelGGL((k_softmax_mfma<U, CW>), dim3(static_cast<unsigned>(per_xcd * NXCD)), dim3(MF_T), 0, s, a,
+                     p.slabs, p.rows_per_slab, per_xcd);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.slabs == 1) return e;
+  const dim3 g2(static_cast<unsigned>((a.d + 63) / 64), static_cast<unsigned>(a.n));
+  hipLaunchKernelGGL(k_slab_reduce_tiles, g2, dim3(256), 0, s, a, p.slabs, U);
+  return hipGetLastError();
+}
+
+template <int CW>
+hipError_t launch_mfma_c(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
+  switch (p.per_thread) {
+    case 1: return launch_mfma_t<1, CW>(p, a, s);
+    case 2: return launch_mfma_t<2, CW>(p, a, s);
+    case 3: return launch_mfma_t<3, CW>(p, a, s);
+    case 4: return launch_mfma_t<4, CW>(p, a, s);
+    case 5: if constexpr (CW <= 10) return launch_mfma_t<5, CW>(p, a, s); break;
+    case 6: if constexpr (CW <= 10) return launch_mfma_t<6, CW>(p, a, s); break;
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int CP>
 hipError_t launch_fused_c(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
   if (p.threads == 256) {
@@ -464,6 +896,31 @@ hipError_t launch_fused_c(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_
 
 SoftmaxPlan softmax_plan(int n, int B, int d, int C) {
   SoftmaxPlan p;
+  {
+    // matrix-core single pass: 8 waves x 64U features, W staged in LDS
+    const int cw = C <= 4 ? 4 : C <= 10 ? 10 : C <= 16 ? 16 : 0;
+    const int U = (d + MF_T - 1) / MF_T;
+    const bool fits = cw == 16 ? U <= 4 : U <= 6;
+    if (cw && d % 4 == 0 && fits) {
+      p.fused = 2;
+      p.threads = MF_T;
+      p.per_thread = U;
+      p.cpad = cw;
+      // about 256 blocks, at least four 8-row chunks per slab
+      int slabs = 256 / n, max_slabs = B / (4 * MF_ROWS);
+      slabs = slabs < 1 ? 1 : slabs;
+      max_slabs = max_slabs < 1 ? 1 : max_slabs;
+      slabs = slabs > max_slabs ? max_slabs : slabs;
+      int rps = (B + slabs - 1) / slabs;
+      rps = (rps + MF_ROWS - 1) / MF_ROWS * MF_ROWS;
+      if (rps > FUSED_MAX_ROWS) rps = FUSED_MAX_ROWS;
+      p.rows_per_slab = rps;
+      p.slabs = (B + rps - 1) / rps;
+      p.part = (int64_t)MF_T * U * C;   // tile-order partial
+      if ((int64_t)p.slabs * p.part * 4 <= kMaxBufferBytes) return p;
+      p = SoftmaxPlan{};
+    }
+  }
   int cp = C <= 4 ? 4 : C <= 10 ? 10 : C <= 16 ? 16 : 0;
   int T = d <= 1024 ? 256 : 512;
   int M = (d + T - 1) / T;
@@ -491,12 +948,21 @@ SoftmaxPlan softmax_plan(int n, int B, int d, int C) {
   p.rows_per_slab = (p.rows_per_slab + 3) / 4 * 4;
   if (p.rows_per_slab > 1024) p.rows_per_slab = 1024;   // rows staged in LDS
   p.slabs = (B + p.rows_per_slab - 1) / p.rows_per_slab;
+  p.part = (int64_t)d * C;
   // one worker's partials are read through one buffer resource
   if ((int64_t)p.slabs * d * C * 4 > kMaxBufferBytes) p.fused = 0;
   return p;
 }
 
 hipError_t launch_softmax_grads(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
+  if (p.fused == 2) {
+    switch (p.cpad) {
+      case 4: return launch_mfma_c<4>(p, a, s);
+      case 10: return launch_mfma_c<10>(p, a, s);
+      case 16: return launch_mfma_c<16>(p, a, s);
+    }
+    return hipErrorInvalidValue;
+  }
   if (p.fused) {
     switch (p.cpad) {
       case 4: return launch_fused_c<4>(p, a, s);

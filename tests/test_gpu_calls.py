@@ -41,6 +41,9 @@ SOFTMAX_SHAPES = [
     (5, 13, 1000, 10),
     (7, 33, 777, 5),
     (2, 9, 3000, 16),
+    (3, 21, 2048, 16),     # 16 classes, 2048 features
+    (5, 37, 1536, 4),      # 4 classes, ragged 8-row chunks
+    (9, 300, 512, 7),      # several row slabs per worker, ragged last slab
     (2, 10, 4500, 10),     # d beyond the fused kernel: GEMM path
     (4, 24, 300, 100),     # 100 classes: GEMM path
     (3, 70, 129, 17),      # GEMM path, ragged tiles
