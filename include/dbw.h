@@ -223,20 +223,26 @@ dbw_status dbw_samples_export(dbw_ctx* ctx, int64_t* cnt, int64_t* tsum, int64_t
 dbw_status dbw_samples_import(dbw_ctx* ctx, const int64_t* cnt, const int64_t* tsum,
                               int64_t clock);
 
-/* Kernel timing with HIP events on the context's stream.  When enabled, every
- * launch of the listed kernel groups is bracketed by events; dbw_kernel_time
- * synchronises and returns the summed milliseconds and the launch count since
- * the last reset.  The two host groups report wall-clock host time (steady
- * clock) spent in the time-estimate solve and in the whole dbw_step call. */
+/* Kernel timing with HIP events on the streams the kernels run on.  With
+ * dbw_profile_enable(ctx, 1) every launch of the device groups is bracketed
+ * by events and the host groups accumulate wall-clock host time (steady
+ * clock); with 2 only the host groups are kept (no events are recorded, so
+ * the host timings are not inflated by them); 0 turns both off.
+ * dbw_kernel_time synchronises and returns the summed milliseconds and the
+ * count since the last reset.  Host groups: the time-estimate solve, the
+ * whole dbw_step call, the part of it spent waiting for the estimate worker,
+ * and the part spent queueing GPU work. */
 typedef enum {
   DBW_KT_GRADS = 0,
   DBW_KT_AGGREGATE = 1,
   DBW_KT_CHOOSE = 2,
   DBW_KT_HOST_ESTIMATE = 3,
   DBW_KT_HOST_STEP = 4,
-  DBW_KT_COUNT = 5
+  DBW_KT_HOST_WAIT = 5,
+  DBW_KT_HOST_QUEUE = 6,
+  DBW_KT_COUNT = 7
 } dbw_kernel_group;
-dbw_status dbw_profile_enable(dbw_ctx* ctx, int32_t on);
+dbw_status dbw_profile_enable(dbw_ctx* ctx, int32_t mode);
 dbw_status dbw_kernel_time(dbw_ctx* ctx, int32_t group, double* total_ms, int64_t* launches);
 dbw_status dbw_profile_reset(dbw_ctx* ctx);
 

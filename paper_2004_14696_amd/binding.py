@@ -21,6 +21,7 @@ DBW_OK, DBW_EINVAL, DBW_ERANGE, DBW_EHIP, DBW_ESTATE, DBW_EUNSUPPORTED = 0, -1, 
 DBW_SOFTMAX, DBW_MLP = 0, 1
 DBW_MAX_N, DBW_MAX_D = 1024, 64
 DBW_KT_GRADS, DBW_KT_AGGREGATE, DBW_KT_CHOOSE, DBW_KT_HOST_ESTIMATE, DBW_KT_HOST_STEP = 0, 1, 2, 3, 4
+DBW_KT_HOST_WAIT, DBW_KT_HOST_QUEUE = 5, 6
 
 STATUS_NAMES = {0: "DBW_OK", -1: "DBW_EINVAL", -2: "DBW_ERANGE", -3: "DBW_EHIP",
                 -4: "DBW_ESTATE", -5: "DBW_EUNSUPPORTED"}
@@ -401,8 +402,10 @@ class Context:
                     "dbw_samples_import")
 
     # -- timing --------------------------------------------------------------------
-    def profile(self, on: bool = True):
-        self._check(self.lib.dbw_profile_enable(self.h, 1 if on else 0), "dbw_profile_enable")
+    def profile(self, on=True):
+        """True/1: device events and host timers; 2: host timers only; False/0: off."""
+        mode = 1 if on is True else (0 if on is False else int(on))
+        self._check(self.lib.dbw_profile_enable(self.h, mode), "dbw_profile_enable")
 
     def profile_reset(self):
         self._check(self.lib.dbw_profile_reset(self.h), "dbw_profile_reset")

@@ -49,6 +49,12 @@ struct dbw_ctx {
   dbw_config cfg{};
   int64_t P = 0;
   hipStream_t stream = nullptr;
+  // Side stream (default priority) for the choice and the statistics of a
+  // step: neither feeds the gradient kernels, so they run beside them.
+  hipStream_t side = nullptr;
+  hipEvent_t ev_agg = nullptr;    // aggregation of the last step (context stream)
+  hipEvent_t ev_fin = nullptr;    // statistics of the last step (side stream)
+  bool side_used = false;         // ev_fin has been recorded
   int device = 0;
   std::string last_error;
   dbw::SoftmaxPlan splan;
@@ -58,7 +64,9 @@ struct dbw_ctx {
   char* pool = nullptr;
   // device buffers (carved from pool)
   float* G = nullptr;
-  float* loss = nullptr;
+  float* loss = nullptr;         // [2][n]: steps alternate (the statistics of
+                                 // step t read it while step t+1's gradients run)
+  float* loss_last = nullptr;    // half written by the last step
   float* g = nullptr;
   uint8_t* mask = nullptr;
   float* sqnorm = nullptr;
@@ -88,7 +96,6 @@ struct dbw_ctx {
   int64_t* d_ticks = nullptr;
   int32_t* d_k = nullptr;
   int32_t* h_err = nullptr;     // [1]
-  hipEvent_t ev[kSlots]{};      // end of the slot's iteration (recorded on request)
   hipEvent_t ev_k[kSlots]{};    // after the slot's choice kernel: k is in h_k
 
   // host bookkeeping of arrival times
@@ -102,6 +109,7 @@ struct dbw_ctx {
   int64_t clock = 0;
   std::vector<double> T_scratch;
   dbw::IsoSolver solver;
+  std::vector<int> pending_rows;  // grid rows changed since the solver's last call
 
   // Estimate worker.  T_hat_{t+1} depends on k_{t-1} only, so it is solved on
   // a host thread of its own while the GPU runs iterations t-1 and t; the
@@ -116,7 +124,8 @@ struct dbw_ctx {
   dbw_status job_status = DBW_OK;
   std::string job_error;
 
-  bool profiling = false;
+  bool profiling = false;      // host timers
+  bool prof_events = false;    // device events
   ProfileGroup prof[DBW_KT_COUNT];
 };
 
@@ -210,6 +219,7 @@ dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
     dbw_status s = known_k(c, u - 1, &h);
     if (s != DBW_OK) return s;
     const std::vector<int64_t>& srt = c->sorted[u % kSlots];
+    c->pending_rows.push_back(h);
     for (int i = 0; i < n; ++i) {
       c->cnt[(size_t)(h - 1) * n + i] += 1;
       c->tsum[(size_t)(h - 1) * n + i] += srt[i];
@@ -249,23 +259,35 @@ dbw_status estimate(dbw_ctx* c, int64_t u) {
   HostScope hs(c, DBW_KT_HOST_ESTIMATE);
   std::string why;
   double* hT = c->h_T + (size_t)(u % kSlots) * c->cfg.n;
-  if (c->solver.solve(c->cfg.n, c->cnt.data(), c->tsum.data(), hT, &why) != 0)
+  if (c->solver.solve(c->cfg.n, c->cnt.data(), c->tsum.data(), hT, &why, &c->pending_rows) != 0)
     return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  c->pending_rows.clear();
   return DBW_OK;
 }
 
 void worker_main(dbw_ctx* c) {
   t_in_worker = true;
   (void)hipSetDevice(c->device);
-  std::unique_lock<std::mutex> lk(c->mu);
   for (;;) {
-    c->cv.wait(lk, [c] { return c->quit || c->job_state.load(std::memory_order_relaxed) == 1; });
-    if (c->quit) return;
-    const int64_t u = c->job_u;
-    lk.unlock();
-    c->job_status = estimate(c, u);
+    // a job usually follows within one step: spin briefly (a sleeping
+    // thread's wake-up costs tens of microseconds), then sleep
+    for (int spin = 0; spin < 20000 && c->job_state.load(std::memory_order_acquire) != 1; ++spin)
+      __builtin_ia32_pause();
+    int64_t u;
+    {
+      std::unique_lock<std::mutex> lk(c->mu);
+      c->cv.wait(lk, [c] { return c->quit || c->job_state.load(std::memory_order_relaxed) == 1; });
+      if (c->quit) return;
+      u = c->job_u;
+    }
+    dbw_status st = DBW_ESTATE;
+    try {
+      st = estimate(c, u);
+    } catch (...) {
+      c->job_error = "time estimate: out of memory";
+    }
+    c->job_status = st;
     c->job_state.store(2, std::memory_order_release);
-    lk.lock();
   }
 }
 
@@ -304,20 +326,36 @@ dbw_status check_device_ptrs(dbw_ctx* c, std::initializer_list<std::pair<const v
 struct ProfScope {
   dbw_ctx* c;
   int g;
+  hipStream_t s;
   bool on;
-  ProfScope(dbw_ctx* ctx, int group) : c(ctx), g(group) {
+  ProfScope(dbw_ctx* ctx, int group, hipStream_t stream = nullptr)
+      : c(ctx), g(group), s(stream ? stream : ctx->stream) {
     ProfileGroup& pg = c->prof[g];
-    on = c->profiling && pg.used < static_cast<int>(pg.start.size());
-    if (on) (void)hipEventRecord(pg.start[pg.used], c->stream);
+    on = c->prof_events && pg.used < static_cast<int>(pg.start.size());
+    if (on) (void)hipEventRecord(pg.start[pg.used], s);
   }
   ~ProfScope() {
     if (on) {
       ProfileGroup& pg = c->prof[g];
-      (void)hipEventRecord(pg.stop[pg.used], c->stream);
+      (void)hipEventRecord(pg.stop[pg.used], s);
       pg.used++;
     }
   }
 };
+
+// Work queued on the context stream after this call sees the last step's
+// side-stream work (statistics, estimator state) complete.
+dbw_status join_side(dbw_ctx* c) {
+  if (c->side_used) HIP_TRY(c, hipStreamWaitEvent(c->stream, c->ev_fin, 0));
+  return DBW_OK;
+}
+
+// Both streams drained.
+dbw_status sync_all(dbw_ctx* c) {
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (c->side) HIP_TRY(c, hipStreamSynchronize(c->side));
+  return DBW_OK;
+}
 
 dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_t* y, const int32_t* rows,
                         float* G, float* loss) {
@@ -411,7 +449,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
     total += (bytes + 255) / 256 * 256;
     return s;
   };
-  Span sG = take(sizeof(float) * n * P), sLoss = take(sizeof(float) * n), sg = take(sizeof(float) * P),
+  Span sG = take(sizeof(float) * n * P), sLoss = take(sizeof(float) * 2 * n), sg = take(sizeof(float) * P),
        sMask = take(n), sSq = take(sizeof(float) * n), sStats = take(sizeof(dbw_iter_stats)),
        sT = take(sizeof(double) * n), sObj = take(sizeof(double) * n), sK = take(4), sB = take(4),
        sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
@@ -439,7 +477,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
     return DBW_EHIP;
   }
   auto at = [&](const Span& s) -> void* { return s.bytes ? c->pool + s.off : nullptr; };
-  c->G = (float*)at(sG); c->loss = (float*)at(sLoss); c->g = (float*)at(sg); c->mask = (uint8_t*)at(sMask);
+  c->G = (float*)at(sG); c->loss = (float*)at(sLoss); c->loss_last = c->loss; c->g = (float*)at(sg); c->mask = (uint8_t*)at(sMask);
   c->sqnorm = (float*)at(sSq); c->stats = (dbw_iter_stats*)at(sStats); c->T_hat = (double*)at(sT);
   c->objective = (double*)at(sObj); c->k = (int32_t*)at(sK); c->b = (int32_t*)at(sB);
   c->sel = (int32_t*)at(sSel); c->ticks = (int64_t*)at(sTicks); c->st = (dbw_estimator_state*)at(sSt);
@@ -456,8 +494,10 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
+  ok = ok && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) == hipSuccess;
+  ok = ok && hipEventCreateWithFlags(&c->ev_agg, hipEventDisableTiming) == hipSuccess;
+  ok = ok && hipEventCreateWithFlags(&c->ev_fin, hipEventDisableTiming) == hipSuccess;
   for (int s = 0; s < kSlots && ok; ++s) {
-    ok = hipEventCreateWithFlags(&c->ev[s], hipEventDisableTiming) == hipSuccess;
     ok = ok && hipEventCreateWithFlags(&c->ev_k[s], hipEventDisableTiming) == hipSuccess;
   }
   if (!ok) {
@@ -501,8 +541,10 @@ DBW_API void dbw_destroy(dbw_ctx* c) {
     c->worker.join();
   }
   if (c->stream || c->pool) (void)hipStreamSynchronize(c->stream);
-  for (auto& ev : c->ev)
-    if (ev) (void)hipEventDestroy(ev);
+  if (c->side) (void)hipStreamSynchronize(c->side);
+  if (c->ev_agg) (void)hipEventDestroy(c->ev_agg);
+  if (c->ev_fin) (void)hipEventDestroy(c->ev_fin);
+  if (c->side) (void)hipStreamDestroy(c->side);
   for (auto& ev : c->ev_k)
     if (ev) (void)hipEventDestroy(ev);
   for (auto& pg : c->prof) {
@@ -520,7 +562,7 @@ DBW_API void dbw_destroy(dbw_ctx* c) {
 DBW_API dbw_status dbw_sync(dbw_ctx* c) {
   if (!c) return DBW_EINVAL;
   DeviceGuard g(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   HIP_TRY(c, hipMemcpy(c->h_err, c->err, sizeof(int32_t), hipMemcpyDeviceToHost));
   const int32_t e = *c->h_err;
   if (e) {
@@ -544,6 +586,7 @@ DBW_API dbw_status dbw_worker_grads(dbw_ctx* c, const float* w, const float* X, 
   if (!aligned16(w) || !aligned16(G)) return fail(c, DBW_EINVAL, "w and G must be 16-byte aligned");
   if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
   DeviceGuard g(c->device);
+  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   return launch_grads(c, w, X, y, rows, G, loss);
 }
 
@@ -554,6 +597,7 @@ DBW_API dbw_status dbw_aggregate_fastest(dbw_ctx* c, const float* G, const int64
     return s;
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
+  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_AGGREGATE);
   dbw::ChooseArgs ca{};
   ca.ticks_src = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
@@ -575,6 +619,7 @@ DBW_API dbw_status dbw_grad_stats(dbw_ctx* c, const float* G, const uint8_t* mas
     return s;
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
+  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_AGGREGATE);
   HIP_TRY(c, dbw::launch_mask_to_sel(mask, c->cfg.n, k, c->sel, c->err, c->stream));
   dbw::AggArgs aa{};
@@ -595,6 +640,7 @@ DBW_API dbw_status dbw_choose_b(dbw_ctx* c, const double* T_hat, int32_t* k_out,
   if (dbw_status s = check_device_ptrs(c, {{T_hat, "T_hat"}, {k_out, "k_out"}, {b_out, "b_out"}}); s != DBW_OK)
     return s;
   DeviceGuard dg(c->device);
+  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_CHOOSE);
   dbw::ChooseArgs ca{};
   ca.st = c->st; ca.T_src = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
@@ -618,12 +664,20 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   HostScope hs_step(c, DBW_KT_HOST_STEP);
   const int64_t t = c->t;
   const int slot = static_cast<int>(t % kSlots);
+  // 0. worker gradients on the context stream first: they need neither the
+  //    time estimate nor the choice, and keep the GPU busy while the host
+  //    waits for T_hat_t.  loss alternates halves by step parity (the
+  //    statistics of step t-1 may still read the other half).
+  float* loss = c->loss + (size_t)(t & 1) * n;
+  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss); s != DBW_OK) return s;
   // 1. T_hat_t in the pinned slot: solved by the worker since k_{t-2} became
   //    known, or here when no job was posted (first step of a history)
   {
+    HostScope hw(c, DBW_KT_HOST_WAIT);
     const bool posted = c->job_state.load(std::memory_order_acquire) != 0;
     if (dbw_status s = posted ? join_estimate(c) : estimate(c, t); s != DBW_OK) return s;
   }
+  HostScope hq(c, DBW_KT_HOST_QUEUE);
   // 2. this iteration's ticks into the pinned slot (its previous reader, the
   //    choice of t-4, precedes the choice of t-2 the estimate waited for)
   int64_t* hk = c->h_ticks + (size_t)slot * n;
@@ -631,40 +685,50 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   std::vector<int64_t>& srt = c->sorted[slot];
   srt.assign(ticks_host, ticks_host + n);
   std::sort(srt.begin(), srt.end());
-  // 3. choose k_t and select the first k_t arrivals; the kernel reads T_hat
-  //    and the ticks from the pinned slot, keeps device copies, and writes
-  //    k_t back into the pinned slot
+  // 3. choose k_t and select the first k_t arrivals on the side stream (after
+  //    the previous step's statistics there); the kernel reads T_hat and the
+  //    ticks from the pinned slot, keeps device copies, and writes k_t back
+  //    into the pinned slot
   {
-    ProfScope ps(c, DBW_KT_CHOOSE);
+    ProfScope ps(c, DBW_KT_CHOOSE, c->side);
     dbw::ChooseArgs ca{};
     ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
     ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.k_host = c->d_k + slot; ca.n = n; ca.eta = c->cfg.eta;
     ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
-    HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+    HIP_TRY(c, dbw::launch_choose_select(ca, c->side));
   }
-  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
-  // 4. worker gradients
-  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, c->loss); s != DBW_OK) return s;
-  // 5. aggregate, statistics, update, estimator bookkeeping
+  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->side));
+  // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored
+  // above, and k_{t-1}); the rest of the queueing overlaps its solve
+  c->t = t + 1;
+  post_estimate(c, t + 1);
+  // 4. aggregate and update once the choice is in, then the statistics and
+  //    the estimator bookkeeping on the side stream
   {
+    HIP_TRY(c, hipStreamWaitEvent(c->stream, c->ev_k[slot], 0));
     ProfScope ps(c, DBW_KT_AGGREGATE);
     dbw::AggArgs aa{};
     aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;
     aa.eta = static_cast<float>(c->cfg.eta); aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_FUSED;
     HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_agg, c->stream));
+  {
+    HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_agg, 0));
+    ProfScope ps(c, DBW_KT_AGGREGATE, c->side);
     dbw::FinalizeArgs fa{};
     fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = c->mask; fa.k_dev = c->k;
-    fa.loss = c->loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;
+    fa.loss = loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;
     fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
-    HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
+    HIP_TRY(c, dbw::launch_finalize(fa, c->side));
   }
-  c->t = t + 1;
-  // 6. T_hat_{t+1} on the worker (it waits for k_{t-1})
-  post_estimate(c, t + 1);
+  HIP_TRY(c, hipEventRecord(c->ev_fin, c->side));
+  c->side_used = true;
+  c->loss_last = loss;
   if (k_host) {
-    HIP_TRY(c, hipEventRecord(c->ev[slot], c->stream));
-    HIP_TRY(c, hipEventSynchronize(c->ev[slot]));
+    // the whole step has completed once the statistics have
+    HIP_TRY(c, hipEventSynchronize(c->ev_fin));
     *k_host = c->h_k[slot];
   }
   return DBW_OK;
@@ -672,7 +736,9 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
 
 DBW_API dbw_status dbw_step_outputs(dbw_ctx* c, dbw_step_buffers* out) {
   if (!c || !out) return DBW_EINVAL;
-  out->G = c->G; out->loss = c->loss; out->g = c->g; out->mask = c->mask; out->sqnorm = c->sqnorm;
+  DeviceGuard dg(c->device);
+  if (dbw_status s = join_side(c); s != DBW_OK) return s;
+  out->G = c->G; out->loss = c->loss_last; out->g = c->g; out->mask = c->mask; out->sqnorm = c->sqnorm;
   out->stats = c->stats; out->T_hat = c->T_hat; out->objective = c->objective; out->k = c->k; out->b = c->b;
   return DBW_OK;
 }
@@ -705,7 +771,7 @@ DBW_API dbw_status dbw_time_estimator_solve(dbw_time_estimator* est, int32_t n, 
 DBW_API dbw_status dbw_state_export(dbw_ctx* c, dbw_estimator_state* out) {
   if (!c || !out) return DBW_EINVAL;
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   HIP_TRY(c, hipMemcpy(out, c->st, sizeof *out, hipMemcpyDeviceToHost));
   return DBW_OK;
 }
@@ -720,7 +786,7 @@ DBW_API dbw_status dbw_state_import(dbw_ctx* c, const dbw_estimator_state* in) {
   if ((in->t == 0) != (in->nV == 0) || in->nF > in->t || in->nV > in->t)
     return fail(c, DBW_EINVAL, "estimator state histories do not match t");
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   // fold what is known before the history restarts
   if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
   HIP_TRY(c, hipMemcpy(c->st, in, sizeof *in, hipMemcpyHostToDevice));
@@ -732,7 +798,7 @@ DBW_API dbw_status dbw_samples_export(dbw_ctx* c, int64_t* cnt, int64_t* tsum, i
   if (!c || !cnt || !tsum || !clock) return DBW_EINVAL;
   if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
   std::memcpy(cnt, c->cnt.data(), sizeof(int64_t) * c->cnt.size());
   std::memcpy(tsum, c->tsum.data(), sizeof(int64_t) * c->tsum.size());
@@ -749,7 +815,7 @@ DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int6
   if (dbw::time_estimate(n, cnt, tsum, probe.data(), &why) != 0)
     return fail(c, DBW_EINVAL, "samples: %s", why.c_str());
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
   std::memcpy(c->cnt.data(), cnt, sizeof(int64_t) * c->cnt.size());
   std::memcpy(c->tsum.data(), tsum, sizeof(int64_t) * c->tsum.size());
@@ -758,11 +824,12 @@ DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int6
   return DBW_OK;
 }
 
-DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
+DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t mode) {
   if (!c) return DBW_EINVAL;
   if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
-  if (on) {
+  if (mode < 0 || mode > 2) return fail(c, DBW_EINVAL, "profile mode must be 0, 1 or 2");
+  if (mode == 1) {
     for (int g = 0; g < DBW_KT_HOST_ESTIMATE; ++g)
       for (auto& pg = c->prof[g]; static_cast<int>(pg.start.size()) < kProfilePairs;) {
         hipEvent_t a, b;
@@ -772,7 +839,8 @@ DBW_API dbw_status dbw_profile_enable(dbw_ctx* c, int32_t on) {
         pg.stop.push_back(b);
       }
   }
-  c->profiling = on != 0;
+  c->profiling = mode != 0;
+  c->prof_events = mode == 1;
   return DBW_OK;
 }
 
@@ -780,7 +848,7 @@ DBW_API dbw_status dbw_kernel_time(dbw_ctx* c, int32_t group, double* total_ms, 
   if (!c || !total_ms || !launches || group < 0 || group >= DBW_KT_COUNT) return DBW_EINVAL;
   if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   ProfileGroup& pg = c->prof[group];
   for (int i = 0; i < pg.used; ++i) {
     float ms = 0.f;
@@ -798,7 +866,7 @@ DBW_API dbw_status dbw_profile_reset(dbw_ctx* c) {
   if (!c) return DBW_EINVAL;
   if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
   DeviceGuard dg(c->device);
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
   for (auto& pg : c->prof) {
     pg.used = 0;
     pg.done_ms = 0.0;

@@ -161,8 +161,12 @@ class IsoSolver {
   ~IsoSolver();
   IsoSolver(const IsoSolver&) = delete;
   IsoSolver& operator=(const IsoSolver&) = delete;
-  // Returns 0 on success, -1 on invalid input (reason in *why).
-  int solve(int n, const int64_t* cnt, const int64_t* tsum, double* T_hat, std::string* why);
+  // Returns 0 on success, -1 on invalid input (reason in *why).  With
+  // changed_rows, the caller guarantees that only those rows (1-based) of the
+  // grid differ from the previous call on this solver, which then validates
+  // and diffs only them.
+  int solve(int n, const int64_t* cnt, const int64_t* tsum, double* T_hat, std::string* why,
+            const std::vector<int>* changed_rows = nullptr);
   void reset();
   int64_t full_solves() const;
   int64_t warm_solves() const;
