@@ -49,12 +49,7 @@ struct dbw_ctx {
   dbw_config cfg{};
   int64_t P = 0;
   hipStream_t stream = nullptr;
-  // Side stream (default priority) for the choice and the statistics of a
-  // step: neither feeds the gradient kernels, so they run beside them.
-  hipStream_t side = nullptr;
-  hipEvent_t ev_agg = nullptr;    // aggregation of the last step (context stream)
-  hipEvent_t ev_fin = nullptr;    // statistics of the last step (side stream)
-  bool side_used = false;         // ev_fin has been recorded
+  hipEvent_t ev_fin = nullptr;    // end of a step (recorded when the caller waits)
   int device = 0;
   std::string last_error;
   dbw::SoftmaxPlan splan;
@@ -64,8 +59,7 @@ struct dbw_ctx {
   char* pool = nullptr;
   // device buffers (carved from pool)
   float* G = nullptr;
-  float* loss = nullptr;         // [2][n]: steps alternate (the statistics of
-                                 // step t read it while step t+1's gradients run)
+  float* loss = nullptr;         // [2][n]: steps alternate halves
   float* loss_last = nullptr;    // half written by the last step
   float* g = nullptr;
   uint8_t* mask = nullptr;
@@ -343,17 +337,8 @@ struct ProfScope {
   }
 };
 
-// Work queued on the context stream after this call sees the last step's
-// side-stream work (statistics, estimator state) complete.
-dbw_status join_side(dbw_ctx* c) {
-  if (c->side_used) HIP_TRY(c, hipStreamWaitEvent(c->stream, c->ev_fin, 0));
-  return DBW_OK;
-}
-
-// Both streams drained.
 dbw_status sync_all(dbw_ctx* c) {
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  if (c->side) HIP_TRY(c, hipStreamSynchronize(c->side));
   return DBW_OK;
 }
 
@@ -494,8 +479,6 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
-  ok = ok && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) == hipSuccess;
-  ok = ok && hipEventCreateWithFlags(&c->ev_agg, hipEventDisableTiming) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_fin, hipEventDisableTiming) == hipSuccess;
   for (int s = 0; s < kSlots && ok; ++s) {
     ok = ok && hipEventCreateWithFlags(&c->ev_k[s], hipEventDisableTiming) == hipSuccess;
@@ -541,10 +524,7 @@ DBW_API void dbw_destroy(dbw_ctx* c) {
     c->worker.join();
   }
   if (c->stream || c->pool) (void)hipStreamSynchronize(c->stream);
-  if (c->side) (void)hipStreamSynchronize(c->side);
-  if (c->ev_agg) (void)hipEventDestroy(c->ev_agg);
   if (c->ev_fin) (void)hipEventDestroy(c->ev_fin);
-  if (c->side) (void)hipStreamDestroy(c->side);
   for (auto& ev : c->ev_k)
     if (ev) (void)hipEventDestroy(ev);
   for (auto& pg : c->prof) {
@@ -586,7 +566,6 @@ DBW_API dbw_status dbw_worker_grads(dbw_ctx* c, const float* w, const float* X, 
   if (!aligned16(w) || !aligned16(G)) return fail(c, DBW_EINVAL, "w and G must be 16-byte aligned");
   if (dbw_status s = check_batch(c, X, y, rows); s != DBW_OK) return s;
   DeviceGuard g(c->device);
-  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   return launch_grads(c, w, X, y, rows, G, loss);
 }
 
@@ -597,7 +576,6 @@ DBW_API dbw_status dbw_aggregate_fastest(dbw_ctx* c, const float* G, const int64
     return s;
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
-  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_AGGREGATE);
   dbw::ChooseArgs ca{};
   ca.ticks_src = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
@@ -619,7 +597,6 @@ DBW_API dbw_status dbw_grad_stats(dbw_ctx* c, const float* G, const uint8_t* mas
     return s;
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
-  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_AGGREGATE);
   HIP_TRY(c, dbw::launch_mask_to_sel(mask, c->cfg.n, k, c->sel, c->err, c->stream));
   dbw::AggArgs aa{};
@@ -640,7 +617,6 @@ DBW_API dbw_status dbw_choose_b(dbw_ctx* c, const double* T_hat, int32_t* k_out,
   if (dbw_status s = check_device_ptrs(c, {{T_hat, "T_hat"}, {k_out, "k_out"}, {b_out, "b_out"}}); s != DBW_OK)
     return s;
   DeviceGuard dg(c->device);
-  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   ProfScope ps(c, DBW_KT_CHOOSE);
   dbw::ChooseArgs ca{};
   ca.st = c->st; ca.T_src = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
@@ -685,49 +661,41 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   std::vector<int64_t>& srt = c->sorted[slot];
   srt.assign(ticks_host, ticks_host + n);
   std::sort(srt.begin(), srt.end());
-  // 3. choose k_t and select the first k_t arrivals on the side stream (after
-  //    the previous step's statistics there); the kernel reads T_hat and the
-  //    ticks from the pinned slot, keeps device copies, and writes k_t back
-  //    into the pinned slot
+  // 3. choose k_t and select the first k_t arrivals; the kernel reads T_hat
+  //    and the ticks from the pinned slot, keeps device copies, and writes
+  //    k_t back into the pinned slot
   {
-    ProfScope ps(c, DBW_KT_CHOOSE, c->side);
+    ProfScope ps(c, DBW_KT_CHOOSE);
     dbw::ChooseArgs ca{};
     ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
     ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.k_host = c->d_k + slot; ca.n = n; ca.eta = c->cfg.eta;
     ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
-    HIP_TRY(c, dbw::launch_choose_select(ca, c->side));
+    HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
   }
-  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->side));
+  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
   // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored
   // above, and k_{t-1}); the rest of the queueing overlaps its solve
   c->t = t + 1;
   post_estimate(c, t + 1);
-  // 4. aggregate and update once the choice is in, then the statistics and
-  //    the estimator bookkeeping on the side stream
+  // 4. aggregate and update, then the statistics and the estimator
+  //    bookkeeping (all on the context stream: the gradient kernel fills
+  //    every CU, so nothing would run beside it)
   {
-    HIP_TRY(c, hipStreamWaitEvent(c->stream, c->ev_k[slot], 0));
     ProfScope ps(c, DBW_KT_AGGREGATE);
     dbw::AggArgs aa{};
     aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;
     aa.eta = static_cast<float>(c->cfg.eta); aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_FUSED;
     HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
-  }
-  HIP_TRY(c, hipEventRecord(c->ev_agg, c->stream));
-  {
-    HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_agg, 0));
-    ProfScope ps(c, DBW_KT_AGGREGATE, c->side);
     dbw::FinalizeArgs fa{};
     fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = c->mask; fa.k_dev = c->k;
     fa.loss = loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;
     fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
-    HIP_TRY(c, dbw::launch_finalize(fa, c->side));
+    HIP_TRY(c, dbw::launch_finalize(fa, c->stream));
   }
-  HIP_TRY(c, hipEventRecord(c->ev_fin, c->side));
-  c->side_used = true;
   c->loss_last = loss;
   if (k_host) {
-    // the whole step has completed once the statistics have
+    HIP_TRY(c, hipEventRecord(c->ev_fin, c->stream));
     HIP_TRY(c, hipEventSynchronize(c->ev_fin));
     *k_host = c->h_k[slot];
   }
@@ -737,7 +705,6 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
 DBW_API dbw_status dbw_step_outputs(dbw_ctx* c, dbw_step_buffers* out) {
   if (!c || !out) return DBW_EINVAL;
   DeviceGuard dg(c->device);
-  if (dbw_status s = join_side(c); s != DBW_OK) return s;
   out->G = c->G; out->loss = c->loss_last; out->g = c->g; out->mask = c->mask; out->sqnorm = c->sqnorm;
   out->stats = c->stats; out->T_hat = c->T_hat; out->objective = c->objective; out->k = c->k; out->b = c->b;
   return DBW_OK;
