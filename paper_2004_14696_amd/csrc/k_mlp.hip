@@ -22,6 +22,7 @@
 
 #include "dbw_buffer.h"
 #include "dbw_internal.h"
+#include "mfma_gemm.h"
 
 namespace dbw {
 namespace {
@@ -123,6 +124,80 @@ __global__ __launch_bounds__(256) void k_mlp_hidden(MlpArgs a) {
       for (int e = 0; e < 4; ++e) {
         const int64_t m = m0 + wm * 32 + mi * 16 + 4 * (lane / 16) + e;
         if (m < Mrows) a.Hh[m * H + nn] = fmaxf(acc[mi][ni][e] + bias, 0.f);
+      }
+    }
+}
+
+// Matrix-core versions on (32 WT)^2 tiles (mfma_gemm.h), used when d and H
+// are multiples of 4 and a worker's rows fit the LDS stage.
+template <int WT>
+__global__ __launch_bounds__(256) void k_mlp_hidden_mfma(MlpArgs a) {
+  constexpr int BM = 32 * WT, NP = mfma_pieces<WT>();
+  __shared__ MfmaLds<WT> L;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int64_t Mrows = (int64_t)a.n * a.B;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const int n0 = blockIdx.x * BM;
+  const int d = a.d, H = a.H;
+  const int64_t xrows = a.rows ? a.S : Mrows;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t ws = make_rsrc(a.w, static_cast<uint32_t>((int64_t)d * H * 4));
+  int64_t xrow[NP];
+#pragma unroll
+  for (int s2 = 0; s2 < NP; ++s2) {
+    const int q = tid + s2 * 256;
+    const int64_t m = m0 + q / 4;
+    xrow[s2] = -1;
+    if (m < Mrows) xrow[s2] = mlp_row(a, static_cast<int>(m / a.B), static_cast<int>(m % a.B), (q % 4) == 0);
+  }
+  mfma_f32x4 acc[WT][WT];
+  mfma_zero<WT>(acc);
+  mfma_gemm_rows_w<WT>(L, xs, xrow, d, ws, H, n0, acc);
+  const float* b1 = a.w + (int64_t)d * H;
+#pragma unroll
+  for (int nt = 0; nt < WT; ++nt) {
+    const int h = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
+    if (h >= H) continue;
+    const float bias = b1[h];
+#pragma unroll
+    for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t m = m0 + wm * 16 * WT + mt * 16 + 4 * (lane >> 4) + r;
+        if (m < Mrows) a.Hh[m * H + h] = fmaxf(acc[mt][nt][r] + bias, 0.f);
+      }
+  }
+}
+
+template <int WT>
+__global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a) {
+  constexpr int BM = 32 * WT;
+  __shared__ MfmaLds<WT> L;
+  __shared__ int sh_row[1024];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int i = blockIdx.z;
+  const int j0 = blockIdx.y * BM, n0 = blockIdx.x * BM;
+  const int d = a.d, H = a.H, B = a.B;
+  const int64_t P = (int64_t)d * H + H + (int64_t)H * a.C + a.C;
+  const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t das = make_rsrc(a.dA + (int64_t)i * B * H, static_cast<uint32_t>((int64_t)B * H * 4));
+  for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(mlp_row(a, i, b, false));
+  __syncthreads();
+  mfma_f32x4 acc[WT][WT];
+  mfma_zero<WT>(acc);
+  mfma_gemm_xt_r<WT>(L, xs, sh_row, d, j0, das, B, H, n0, acc);
+  float* Gi = a.G + (int64_t)i * P;
+#pragma unroll
+  for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + wm * 16 * WT + mt * 16 + 4 * (lane >> 4) + r;
+      if (j >= d) continue;
+#pragma unroll
+      for (int nt = 0; nt < WT; ++nt) {
+        const int h = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
+        if (h < H) Gi[(int64_t)j * H + h] = acc[mt][nt][r];
       }
     }
 }
@@ -372,8 +447,16 @@ MlpPlan mlp_plan(int n, int B, int d, int H, int C) {
 hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& a, hipStream_t s) {
   if (!p.ok) return hipErrorNotSupported;
   const int64_t Mrows = (int64_t)a.n * a.B;
-  hipLaunchKernelGGL(k_mlp_hidden, dim3((a.H + TN - 1) / TN, static_cast<unsigned>((Mrows + TM - 1) / TM)), dim3(256),
-                     0, s, a);
+  const bool big = a.d % 4 == 0 && a.H % 4 == 0 && a.B <= 1024;
+  if (big && (int64_t)((a.H + 127) / 128) * ((Mrows + 127) / 128) >= kMfmaBigTiles)
+    hipLaunchKernelGGL(k_mlp_hidden_mfma<4>, dim3((a.H + 127) / 128, static_cast<unsigned>((Mrows + 127) / 128)),
+                       dim3(256), 0, s, a);
+  else if (big)
+    hipLaunchKernelGGL(k_mlp_hidden_mfma<2>, dim3((a.H + 63) / 64, static_cast<unsigned>((Mrows + 63) / 64)),
+                       dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_mlp_hidden, dim3((a.H + TN - 1) / TN, static_cast<unsigned>((Mrows + TM - 1) / TM)),
+                       dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   switch (p.cpad * 100 + p.per_thread * 10 + (p.threads == 512)) {
@@ -390,7 +473,12 @@ hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& a, hipStream_t s) {
     default: return hipErrorNotSupported;
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_mlp_dw1, dim3((a.H + TN - 1) / TN, (a.d + TM - 1) / TM, a.n), dim3(256), 0, s, a);
+  if (big && (int64_t)((a.H + 127) / 128) * ((a.d + 127) / 128) * a.n >= kMfmaBigTiles)
+    hipLaunchKernelGGL(k_mlp_dw1_mfma<4>, dim3((a.H + 127) / 128, (a.d + 127) / 128, a.n), dim3(256), 0, s, a);
+  else if (big)
+    hipLaunchKernelGGL(k_mlp_dw1_mfma<2>, dim3((a.H + 63) / 64, (a.d + 63) / 64, a.n), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_mlp_dw1, dim3((a.H + TN - 1) / TN, (a.d + TM - 1) / TM, a.n), dim3(256), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_mlp_tail, dim3(static_cast<unsigned>((p.tail + 255) / 256), a.n), dim3(256), 0, s, a,

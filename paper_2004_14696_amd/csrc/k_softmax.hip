@@ -27,6 +27,7 @@
 
 #include "dbw_buffer.h"
 #include "dbw_internal.h"
+#include "mfma_gemm.h"
 
 namespace dbw {
 namespace {
@@ -832,6 +833,96 @@ __global__ __launch_bounds__(256) void k_grads_gemm(SoftmaxArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core fp32 GEMMs for the large-C path (C % 4 == 0, d % 4 == 0):
+// 128 x 128 tiles, or 64 x 64 when the large tiles cannot fill the chip;
+// main loops in mfma_gemm.h.
+
+// Z[m][c] = sum_j X[row(m)][j] W[j][c]; blockIdx.x = class tile, y = row tile.
+template <int WT>
+__global__ __launch_bounds__(256) void k_logits_mfma(SoftmaxArgs a) {
+  constexpr int BM = 32 * WT, NP = mfma_pieces<WT>();
+  __shared__ MfmaLds<WT> L;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int64_t Mrows = (int64_t)a.n * a.B;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const int n0 = blockIdx.x * BM;
+  const int d = a.d, C = a.C;
+  const int64_t xrows = a.rows ? a.S : Mrows;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t ws = make_rsrc(a.W, static_cast<uint32_t>((int64_t)d * C * 4));
+  int64_t xrow[NP];
+#pragma unroll
+  for (int s2 = 0; s2 < NP; ++s2) {
+    const int q = tid + s2 * 256;
+    const int64_t m = m0 + q / 4;
+    xrow[s2] = -1;
+    if (m < Mrows) xrow[s2] = sample_row(a, static_cast<int>(m / a.B), static_cast<int>(m % a.B), (q % 4) == 0);
+  }
+  mfma_f32x4 acc[WT][WT];
+  mfma_zero<WT>(acc);
+  mfma_gemm_rows_w<WT>(L, xs, xrow, d, ws, C, n0, acc);
+#pragma unroll
+  for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t m = m0 + wm * 16 * WT + mt * 16 + 4 * (lane >> 4) + r;
+      if (m >= Mrows) continue;
+#pragma unroll
+      for (int nt = 0; nt < WT; ++nt) {
+        const int c = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
+        if (c < C) a.Z[m * C + c] = acc[mt][nt][r];
+      }
+    }
+}
+
+// G_i[j][c] = sum_b X[row(i,b)][j] R_i[b][c]; blockIdx.x = class tile,
+// y = feature tile, z = worker.  Block (0, 0, i) also writes loss_i.
+template <int WT>
+__global__ __launch_bounds__(256) void k_grads_mfma(SoftmaxArgs a) {
+  constexpr int BM = 32 * WT;
+  __shared__ MfmaLds<WT> L;
+  __shared__ int sh_row[FUSED_MAX_ROWS];
+  __shared__ float sh[256];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int i = blockIdx.z;
+  const int j0 = blockIdx.y * BM, n0 = blockIdx.x * BM;
+  const int d = a.d, C = a.C, B = a.B;
+  const int64_t P = (int64_t)d * C;
+  const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.Z + (int64_t)i * B * C, static_cast<uint32_t>((int64_t)B * C * 4));
+  for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(sample_row(a, i, b, false));
+  __syncthreads();
+  mfma_f32x4 acc[WT][WT];
+  mfma_zero<WT>(acc);
+  mfma_gemm_xt_r<WT>(L, xs, sh_row, d, j0, rs, B, C, n0, acc);
+#pragma unroll
+  for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + wm * 16 * WT + mt * 16 + 4 * (lane >> 4) + r;
+      if (j >= d) continue;
+#pragma unroll
+      for (int nt = 0; nt < WT; ++nt) {
+        const int c = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
+        if (c < C) a.G[(int64_t)i * P + (int64_t)j * C + c] = acc[mt][nt][r];
+      }
+    }
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    // loss_i = mean CE over the worker's rows (fixed order)
+    float s = 0.f;
+    for (int b = tid; b < B; b += 256) s += a.ce[(int64_t)i * B + b];
+    sh[tid] = s;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (tid < st) sh[tid] += sh[tid + st];
+      __syncthreads();
+    }
+    if (tid == 0) a.loss[i] = sh[0] / static_cast<float>(B);
+  }
+}
+
 template <int CP, int M, int T>
 hipError_t launch_fused_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
   constexpr int R = 4;
@@ -972,15 +1063,40 @@ hipError_t launch_softmax_grads(const SoftmaxPlan& p, const SoftmaxArgs& a, hipS
     return hipErrorInvalidValue;
   }
   const int64_t Mrows = (int64_t)a.n * a.B;
-  dim3 g1((a.C + GBN - 1) / GBN, static_cast<unsigned>((Mrows + GBM - 1) / GBM));
-  hipLaunchKernelGGL(k_logits_gemm, g1, dim3(256), 0, s, a);
+  // matrix cores when float4 pieces tile the rows of X, W and R exactly
+  // (and a worker's row indices fit the LDS stage)
+  const bool mfma = a.C % 4 == 0 && a.d % 4 == 0 && a.B <= FUSED_MAX_ROWS;
+  if (mfma) {
+    const int64_t tiles = (int64_t)((a.C + 127) / 128) * ((Mrows + 127) / 128);
+    if (tiles >= kMfmaBigTiles) {
+      dim3 g1((a.C + 127) / 128, static_cast<unsigned>((Mrows + 127) / 128));
+      hipLaunchKernelGGL(k_logits_mfma<4>, g1, dim3(256), 0, s, a);
+    } else {
+      dim3 g1((a.C + 63) / 64, static_cast<unsigned>((Mrows + 63) / 64));
+      hipLaunchKernelGGL(k_logits_mfma<2>, g1, dim3(256), 0, s, a);
+    }
+  } else {
+    dim3 g1((a.C + GBN - 1) / GBN, static_cast<unsigned>((Mrows + GBM - 1) / GBM));
+    hipLaunchKernelGGL(k_logits_gemm, g1, dim3(256), 0, s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_rows_softmax, dim3(static_cast<unsigned>((Mrows + 3) / 4)), dim3(256), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 g3((a.C + GBN - 1) / GBN, (a.d + GBM - 1) / GBM, a.n);
-  hipLaunchKernelGGL(k_grads_gemm, g3, dim3(256), 0, s, a);
+  if (mfma) {
+    const int64_t tiles = (int64_t)((a.C + 127) / 128) * ((a.d + 127) / 128) * a.n;
+    if (tiles >= kMfmaBigTiles) {
+      dim3 g3((a.C + 127) / 128, (a.d + 127) / 128, a.n);
+      hipLaunchKernelGGL(k_grads_mfma<4>, g3, dim3(256), 0, s, a);
+    } else {
+      dim3 g3((a.C + 63) / 64, (a.d + 63) / 64, a.n);
+      hipLaunchKernelGGL(k_grads_mfma<2>, g3, dim3(256), 0, s, a);
+    }
+  } else {
+    dim3 g3((a.C + GBN - 1) / GBN, (a.d + GBM - 1) / GBM, a.n);
+    hipLaunchKernelGGL(k_grads_gemm, g3, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

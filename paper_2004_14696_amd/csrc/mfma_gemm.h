@@ -1,0 +1,157 @@
+// fp32 matrix-core GEMM main loops shared by the softmax and MLP kernels.
+//
+// One block (256 threads = four waves in 2 x 2) computes a (32 WT)^2 output
+// tile; each wave owns a (16 WT)^2 = WT x WT set of v_mfma_f32_16x16x4f32
+// tiles (WT = 4: 128 x 128 blocks for large outputs; WT = 2: 64 x 64 blocks
+// when the output has too few large tiles to fill the 256 CUs).
+// K advances 16 at a time through two LDS buffers laid out [k][m] / [k][n],
+// so that the A operand of lane l (row l % 16, k l / 16) and its B operand
+// (k l / 16, column l % 16) are single conflict-free LDS reads; the next
+// slice's global loads (float4 buffer loads, 0 out of range) are in flight
+// while the current one is multiplied.  Accumulator element r of lane l in
+// tile (mt, nt) is output (row 16 mt + 4 (l / 16) + r, column 16 nt + l % 16)
+// of the wave's (16 WT)^2.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "dbw_buffer.h"
+
+namespace dbw {
+
+typedef float mfma_f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int MBK = 16, MPAD = 4;
+
+// Below this many 128 x 128 output tiles (two per CU) a launch uses 64 x 64
+// blocks instead.
+constexpr int64_t kMfmaBigTiles = 512;
+
+template <int WT>
+struct MfmaLds {
+  static constexpr int BM = 32 * WT;
+  float A[2][MBK][BM + MPAD];
+  float B[2][MBK][BM + MPAD];
+};
+
+template <int WT>
+__device__ __forceinline__ void mfma_zero(mfma_f32x4 (&acc)[WT][WT]) {
+#pragma unroll
+  for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < WT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+template <int WT>
+__device__ __forceinline__ void mfma_slice(const MfmaLds<WT>& L, int cbuf, int wm, int wn, int lane,
+                                           mfma_f32x4 (&acc)[WT][WT]) {
+  const int i = lane & 15, kq = lane >> 4;
+#pragma unroll
+  for (int ks = 0; ks < MBK; ks += 4) {
+    float av[WT], bv[WT];
+#pragma unroll
+    for (int t = 0; t < WT; ++t) {
+      av[t] = L.A[cbuf][ks + kq][wm * 16 * WT + t * 16 + i];
+      bv[t] = L.B[cbuf][ks + kq][wn * 16 * WT + t * 16 + i];
+    }
+#pragma unroll
+    for (int mt = 0; mt < WT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < WT; ++nt) acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+  }
+}
+
+// Pieces per thread of one K slice: the A and the B slice each hold 16 BM
+// floats = 4 BM float4 pieces over 256 threads.
+template <int WT>
+constexpr int mfma_pieces() { return 32 * WT / 64; }
+
+// acc += X[row(m0 + r)][k] W[k][n0 + c] over k < K, for the block's tile.
+// xrow[s] is the dataset row of tile row (tid + 256 s) / 4, or -1 for rows
+// past the matrix; W is K x N row-major (N % 4 == 0, K % 4 == 0).
+template <int WT>
+__device__ __forceinline__ void mfma_gemm_rows_w(MfmaLds<WT>& L, __amdgpu_buffer_rsrc_t xs,
+                                                 const int64_t (&xrow)[mfma_pieces<WT>()], int K,
+                                                 __amdgpu_buffer_rsrc_t ws, int N, int n0, mfma_f32x4 (&acc)[WT][WT]) {
+  constexpr int NP = mfma_pieces<WT>(), BQ = 8 * WT;   // B pieces per K row
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  auto load = [&](int k0, float4 (&ra)[NP], float4 (&rb)[NP]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NP; ++s2) {
+      const int q = tid + s2 * 256;
+      const int k = k0 + 4 * (q % 4);
+      ra[s2] = buf_f32x4(xs, xrow[s2] >= 0 && k < K ? static_cast<uint32_t>((xrow[s2] * K + k) * 4) : kOutOfRange);
+      const int kb = k0 + q / BQ, nb = n0 + 4 * (q % BQ);
+      rb[s2] = buf_f32x4(ws, kb < K && nb < N ? static_cast<uint32_t>(((int64_t)kb * N + nb) * 4) : kOutOfRange);
+    }
+  };
+  auto store = [&](int buf, const float4 (&ra)[NP], const float4 (&rb)[NP]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NP; ++s2) {
+      const int q = tid + s2 * 256;
+      const int r = q / 4, k = 4 * (q % 4);
+      L.A[buf][k + 0][r] = ra[s2].x;
+      L.A[buf][k + 1][r] = ra[s2].y;
+      L.A[buf][k + 2][r] = ra[s2].z;
+      L.A[buf][k + 3][r] = ra[s2].w;
+      *reinterpret_cast<float4*>(&L.B[buf][q / BQ][4 * (q % BQ)]) = rb[s2];
+    }
+  };
+  float4 ra[NP], rb[NP];
+  load(0, ra, rb);
+  store(0, ra, rb);
+  __syncthreads();
+  const int nk = (K + MBK - 1) / MBK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cbuf = kt & 1;
+    if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
+    mfma_slice(L, cbuf, wm, wn, lane, acc);
+    if (kt + 1 < nk) store(cbuf ^ 1, ra, rb);
+    __syncthreads();
+  }
+}
+
+// acc += X[srow[b]][j0 + r] R[b][n0 + c] over b < K (the transpose of a
+// worker's rows times its K x N residual block R, row-major; J features per
+// dataset row, J % 4 == 0, N % 4 == 0).  srow holds the worker's K dataset
+// rows (LDS).
+template <int WT>
+__device__ __forceinline__ void mfma_gemm_xt_r(MfmaLds<WT>& L, __amdgpu_buffer_rsrc_t xs, const int* srow, int J,
+                                               int j0, __amdgpu_buffer_rsrc_t rs, int K, int N, int n0,
+                                               mfma_f32x4 (&acc)[WT][WT]) {
+  constexpr int NP = mfma_pieces<WT>(), BQ = 8 * WT;   // pieces per K row (A and B)
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  auto load = [&](int k0, float4 (&ra)[NP], float4 (&rb)[NP]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NP; ++s2) {
+      const int q = tid + s2 * 256;
+      const int b = k0 + q / BQ, j = j0 + 4 * (q % BQ), c = n0 + 4 * (q % BQ);
+      ra[s2] = buf_f32x4(xs, b < K && j < J ? static_cast<uint32_t>(((int64_t)srow[b] * J + j) * 4) : kOutOfRange);
+      rb[s2] = buf_f32x4(rs, b < K && c < N ? static_cast<uint32_t>(((int64_t)b * N + c) * 4) : kOutOfRange);
+    }
+  };
+  auto store = [&](int buf, const float4 (&ra)[NP], const float4 (&rb)[NP]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NP; ++s2) {
+      const int q = tid + s2 * 256;
+      *reinterpret_cast<float4*>(&L.A[buf][q / BQ][4 * (q % BQ)]) = ra[s2];
+      *reinterpret_cast<float4*>(&L.B[buf][q / BQ][4 * (q % BQ)]) = rb[s2];
+    }
+  };
+  float4 ra[NP], rb[NP];
+  load(0, ra, rb);
+  store(0, ra, rb);
+  __syncthreads();
+  const int nk = (K + MBK - 1) / MBK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cbuf = kt & 1;
+    if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
+    mfma_slice(L, cbuf, wm, wn, lane, acc);
+    if (kt + 1 < nk) store(cbuf ^ 1, ra, rb);
+    __syncthreads();
+  }
+}
+
+}  // namespace dbw

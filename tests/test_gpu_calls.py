@@ -45,8 +45,10 @@ SOFTMAX_SHAPES = [
     (5, 37, 1536, 4),      # 4 classes, ragged 8-row chunks
     (9, 300, 512, 7),      # several row slabs per worker, ragged last slab
     (2, 10, 4500, 10),     # d beyond the fused kernel: GEMM path
-    (4, 24, 300, 100),     # 100 classes: GEMM path
-    (3, 70, 129, 17),      # GEMM path, ragged tiles
+    (4, 24, 300, 100),     # 100 classes: GEMM path on the matrix cores
+    (5, 33, 1000, 64),     # matrix-core GEMMs, ragged row tiles
+    (3, 40, 260, 132),     # two class tiles
+    (3, 70, 129, 17),      # GEMM path on the vector ALUs, ragged tiles
 ]
 
 
@@ -119,6 +121,8 @@ MLP_SHAPES = [
     (32, 64, 784, 512, 10),   # 32 workers x 64 rows, 784-512-10
     (3, 7, 50, 40, 3),
     (2, 5, 100, 300, 10),     # hidden width not a multiple of the block
+    (3, 21, 260, 200, 10),    # matrix-core tiles, ragged in rows, features and units
+    (16, 1000, 36, 512, 10),  # enough rows for 128 x 128 hidden-layer tiles
     (5, 13, 70, 600, 10),     # two hidden units per head thread
     (4, 9, 33, 17, 16),
     (1, 1, 3, 5, 2),
