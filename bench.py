@@ -29,15 +29,21 @@ if ROOT not in sys.path:
 
 METRIC = "worker-gradient samples/sec per DBW iteration (1 MI355X); % peak HBM GB/s"
 HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
+FUSED_MAX_CLASSES = 16         # the single-pass softmax kernel covers C <= 16
 
 
-TRAFFIC_FILE = {"C3": "profiles/traffic_worker_grads_softmax_n64_B256_d3072_C10.md"}
+TRAFFIC_FILE = {
+    "C3": "profiles/traffic_worker_grads_softmax_n64_B256_d3072_C10.md",
+    "C4": "profiles/traffic_worker_grads_mlp_n32_B64_784_512_10.md",
+    "C5": "profiles/traffic_worker_grads_softmax_n256_B512_d3072_C100.md",
+}
 
 
 def measured_traffic(cfg):
     """HBM bytes per gradient launch from the committed counter summary, or
-    None when there is none for this workload or the kernel source changed
-    since it was taken."""
+    None when there is none for this workload or a kernel source it covers
+    changed since it was taken."""
     import hashlib
     import os
     path = TRAFFIC_FILE.get(cfg.name)
@@ -50,9 +56,10 @@ def measured_traffic(cfg):
             rec = json.loads(line.split(":", 1)[1])
     if rec is None:
         return None
-    src = os.path.join(root, rec["kernel_source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
-        return None
+    for src, digest in rec["kernel_sources_sha256"].items():
+        with open(os.path.join(root, src), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
     return rec["traffic_bytes_per_launch"]
 
 
@@ -62,6 +69,24 @@ def grads_bytes(cfg, P: int, gathered: bool) -> int:
     and losses written."""
     rows = cfg.n * cfg.B
     return 4 * (rows * cfg.d + rows + (rows if gathered else 0) + P + cfg.n * P + cfg.n)
+
+
+def grads_flops(cfg) -> float:
+    """Useful fp32 flops of one worker-gradient launch (no padding): softmax
+    logits X W and gradient X^T R; MLP hidden layer, head forward, head
+    backward (dW2 and the hidden-unit residuals) and X^T dA."""
+    M = cfg.n * cfg.B
+    if cfg.model == "softmax":
+        return 4.0 * M * cfg.d * cfg.C
+    return 4.0 * M * cfg.d * cfg.H + 6.0 * M * cfg.H * cfg.C
+
+
+def roofline_bound(cfg) -> str:
+    """The single-pass softmax kernel streams each row once and is bounded by
+    HBM; the two-GEMM large-class path and the MLP are fp32 matrix-core work."""
+    if cfg.model == "softmax" and cfg.C <= FUSED_MAX_CLASSES:
+        return "hbm"
+    return "mfma"
 
 
 def step_bytes(cfg, P: int, k: int, gathered: bool) -> int:
@@ -109,6 +134,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="skip the per-launch HIP events (the roofline fields are then omitted)")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for hardware-counter passes: three 256 MiB device copies (the calibration), "
+                         "then five gradient launches of the workload; prints no bench line")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the DBW hot path here simulates all n workers on a single "
@@ -124,6 +152,12 @@ def main(argv=None) -> int:
     cfg = get(args.workload)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
+    if args.traffic_probe:
+        src = torch.full((64 * 1024 * 1024,), 1.0, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     X, y = gen.dataset(cfg)
     Xd = torch.from_numpy(np.ascontiguousarray(X)).to(dev)
     yd = torch.from_numpy(np.ascontiguousarray(y)).to(dev)
@@ -134,6 +168,15 @@ def main(argv=None) -> int:
     w = torch.from_numpy(init_params(cfg)).to(dev)
     ctx = dbw.Context(dbw.config_from(cfg, S=cfg.S))
     P = ctx.P
+
+    if args.traffic_probe:
+        G = torch.empty((cfg.n, P), dtype=torch.float32, device=dev)
+        Lb = torch.empty(cfg.n, dtype=torch.float32, device=dev)
+        for t in range(5):
+            ctx.worker_grads(w, Xd, yd, rows=rows[t % len(rows)], G=G, loss=Lb)
+        ctx.sync()
+        print(f"traffic probe: 3 copies of 256 MiB, 5 gradient launches of {cfg.name}", flush=True)
+        return 0
 
     ks = []
     for t in range(args.warmup):
@@ -189,7 +232,11 @@ def main(argv=None) -> int:
     value = cfg.n * cfg.B / (ms_per_step / 1e3)
     gb = grads_bytes(cfg, P, True)
     grads_avg_s = grads_ms / max(grads_n, 1) / 1e3 if grads_n else float("nan")
-    achieved = gb / grads_avg_s / 1e9
+    bound = roofline_bound(cfg)
+    if bound == "hbm":
+        achieved, peak, unit = gb / grads_avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved, peak, unit = grads_flops(cfg) / grads_avg_s / 1e12, MFMA_F32_PEAK_TFLOPS, "TFLOP/s"
     sb = step_bytes(cfg, P, k_last, True)
     out = {
         "metric": METRIC,
@@ -213,13 +260,14 @@ def main(argv=None) -> int:
         },
         "roofline": {
             "kernel": "worker gradients (dbw_worker_grads)",
-            "bound": "hbm",
+            "bound": bound,
             "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
+            "peak": peak,
+            "unit": unit,
+            "frac": achieved / peak,
             "traffic": measured_traffic(cfg),
             "bytes_per_launch": gb,
+            "flops_per_launch": grads_flops(cfg),
             "avg_launch_ms": grads_avg_s * 1e3,
             "launches": grads_n,
         },
