@@ -210,6 +210,12 @@ dbw_status dbw_time_estimator_create(dbw_time_estimator** out);
 void dbw_time_estimator_destroy(dbw_time_estimator* est);
 dbw_status dbw_time_estimator_solve(dbw_time_estimator* est, int32_t n, const int64_t* cnt,
                                     const int64_t* tsum, double* T_hat);
+/* How the estimator's solves so far were obtained (diagnostics; HOST int64
+ * outs, each may be NULL): fast = exact per-column fits that satisfied every
+ * other relation of Eq. quadratic_opt, warm = re-certified and repaired
+ * previous solutions, full = solves from scratch.  A solve with no sampled
+ * cell counts in none of them.  DBW_EINVAL for a NULL estimator. */
+dbw_status dbw_time_estimator_stats(const dbw_time_estimator* est, int64_t* fast, int64_t* warm, int64_t* full);
 
 /* Estimator state transfer (resume, lockstep testing).  HOST structs; both
  * calls synchronise the context's stream. */

@@ -32,7 +32,7 @@ EXPORTED = (
     "dbw_step_outputs", "dbw_time_estimate", "dbw_state_export", "dbw_state_import",
     "dbw_samples_export", "dbw_samples_import", "dbw_profile_enable", "dbw_kernel_time",
     "dbw_profile_reset", "dbw_time_estimator_create", "dbw_time_estimator_destroy",
-    "dbw_time_estimator_solve",
+    "dbw_time_estimator_solve", "dbw_time_estimator_stats",
 )
 
 
@@ -107,6 +107,8 @@ def load_library(path: str = LIB_PATH):
     lib.dbw_time_estimator_destroy.restype = None
     lib.dbw_time_estimator_solve.argtypes = [P, c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_double)]
     lib.dbw_time_estimator_solve.restype = st
+    lib.dbw_time_estimator_stats.argtypes = [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)]
+    lib.dbw_time_estimator_stats.restype = st
     lib.dbw_state_export.argtypes = [P, POINTER(EstimatorState)]
     lib.dbw_state_export.restype = st
     lib.dbw_state_import.argtypes = [P, POINTER(EstimatorState)]
@@ -178,6 +180,14 @@ class TimeEstimator:
         if s != DBW_OK:
             raise DBWError(s, "dbw_time_estimator_solve rejected its input")
         return out
+
+    def stats(self) -> dict:
+        """Solves so far by path: fast (per-column fit feasible), warm, full."""
+        f, w, u = c_int64(), c_int64(), c_int64()
+        s = self.lib.dbw_time_estimator_stats(self.h, ctypes.byref(f), ctypes.byref(w), ctypes.byref(u))
+        if s != DBW_OK:
+            raise DBWError(s, "dbw_time_estimator_stats failed")
+        return {"fast": f.value, "warm": w.value, "full": u.value}
 
     def __del__(self):
         if getattr(self, "h", None):

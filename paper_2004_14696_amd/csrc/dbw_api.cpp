@@ -735,6 +735,15 @@ DBW_API dbw_status dbw_time_estimator_solve(dbw_time_estimator* est, int32_t n, 
   return est->solver.solve(n, cnt, tsum, T_hat, &why) == 0 ? DBW_OK : DBW_EINVAL;
 }
 
+DBW_API dbw_status dbw_time_estimator_stats(const dbw_time_estimator* est, int64_t* fast, int64_t* warm,
+                                            int64_t* full) {
+  if (!est) return DBW_EINVAL;
+  if (fast) *fast = est->solver.fast_solves();
+  if (warm) *warm = est->solver.warm_solves();
+  if (full) *full = est->solver.full_solves();
+  return DBW_OK;
+}
+
 DBW_API dbw_status dbw_state_export(dbw_ctx* c, dbw_estimator_state* out) {
   if (!c || !out) return DBW_EINVAL;
   DeviceGuard dg(c->device);

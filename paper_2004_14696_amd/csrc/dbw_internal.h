@@ -170,6 +170,7 @@ class IsoSolver {
   void reset();
   int64_t full_solves() const;
   int64_t warm_solves() const;
+  int64_t fast_solves() const;
 
  private:
   struct Impl;

@@ -167,3 +167,57 @@ def test_incremental_estimator_handles_arbitrary_changes(lib):
         rows = sorted(set(int(x) for x in rng.integers(1, n + 1, size=int(rng.integers(1, 4)))))
         cnt, tsum = _grid(rng, n, rows, int(rng.integers(1, 5)), full=bool(rng.random() < 0.5), law="small")
         np.testing.assert_array_equal(est.solve(cnt, tsum), pb.time_estimate(cnt, tsum))
+
+
+def _fold_rows(rng, n, iters, scale, ks=None):
+    """Grid after each iteration of a trajectory whose iteration-t arrivals
+    (n sorted shifted-exponential times, scaled by scale(h)) land in row
+    h = k_{t-1}; k_t drawn from ks (default: uniform on 1..n)."""
+    cnt = np.zeros((n, n), np.int64)
+    tsum = np.zeros((n, n), np.int64)
+    h = n
+    for _ in range(iters):
+        tau = (1 + rng.exponential(1.0, size=n)) * scale(h)
+        cnt[h - 1] += 1
+        tsum[h - 1] += np.sort(np.rint(tau * 2 ** 20).astype(np.int64))
+        yield cnt, tsum
+        h = int(rng.choice(ks)) if ks is not None else int(rng.integers(1, n + 1))
+
+
+def test_estimator_column_fast_path_on_fresh_clock_samples(lib):
+    # With every row drawn from one law (each iteration starts all workers
+    # afresh) and the choices concentrated on a few k, as DBW's are, the
+    # per-column fit is feasible and taken nearly always; it must still be
+    # the exact optimum.
+    rng = np.random.default_rng(45)
+    est = pb.TimeEstimator()
+    n, iters = 32, 60
+    for cnt, tsum in _fold_rows(rng, n, iters, lambda h: 1.0, ks=[1, 2, 16, 32]):
+        got = est.solve(cnt, tsum)
+        ref = te.time_estimate(cnt.tolist(), tsum.tolist())
+        for k in range(n):
+            if ref[k] is None:
+                assert math.isnan(got[k])
+            else:
+                assert got[k] == pytest.approx(ref[k], rel=1e-14, abs=0), k
+    st = est.stats()
+    assert st["fast"] >= 0.9 * iters, st
+
+
+def test_estimator_falls_back_when_the_diagonal_binds(lib):
+    # Rows whose times shrink with h break x_{k,k} <= x_{k+1,k+1} in the
+    # per-column fit: the warm or full solver must take over, exactly.
+    rng = np.random.default_rng(46)
+    est = pb.TimeEstimator()
+    n, iters = 16, 50
+    for cnt, tsum in _fold_rows(rng, n, iters, lambda h: 3.0 - 2.5 * h / 16):
+        got = est.solve(cnt, tsum)
+        ref = te.time_estimate(cnt.tolist(), tsum.tolist())
+        for k in range(n):
+            if ref[k] is None:
+                assert math.isnan(got[k])
+            else:
+                assert got[k] == pytest.approx(ref[k], rel=1e-14, abs=0), k
+        np.testing.assert_array_equal(got, pb.time_estimate(cnt, tsum))
+    st = est.stats()
+    assert st["warm"] + st["full"] > 0, st
