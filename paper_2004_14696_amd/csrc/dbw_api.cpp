@@ -85,12 +85,14 @@ struct dbw_ctx {
   // pinned host staging (coherent; kernels read and write it in place)
   double* h_T = nullptr;        // [kSlots][n]
   int64_t* h_ticks = nullptr;   // [kSlots][n]
+  int32_t* h_order = nullptr;   // [kSlots][n] workers by (tick, index)
   int32_t* h_k = nullptr;       // [kSlots]
   double* d_T = nullptr;        // device-side addresses of the three above
   int64_t* d_ticks = nullptr;
+  int32_t* d_order = nullptr;
   int32_t* d_k = nullptr;
   int32_t* h_err = nullptr;     // [1]
-  hipEvent_t ev_k[kSlots]{};    // after the slot's choice kernel: k is in h_k
+  hipEvent_t ev_k[kSlots]{};    // after the slot's PS kernel: k is in h_k
 
   // host bookkeeping of arrival times
   int64_t t = 0;                // next iteration index (== device state t once drained)
@@ -474,9 +476,11 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   const unsigned pin = hipHostMallocMapped | hipHostMallocCoherent;
   ok = ok && hipHostMalloc((void**)&c->h_T, sizeof(double) * kSlots * n, pin) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_ticks, sizeof(int64_t) * kSlots * n, pin) == hipSuccess;
+  ok = ok && hipHostMalloc((void**)&c->h_order, sizeof(int32_t) * kSlots * n, pin) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_k, sizeof(int32_t) * kSlots, pin) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_T, c->h_T, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
+  ok = ok && hipHostGetDevicePointer((void**)&c->d_order, c->h_order, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_fin, hipEventDisableTiming) == hipSuccess;
@@ -533,6 +537,7 @@ DBW_API void dbw_destroy(dbw_ctx* c) {
   }
   if (c->h_T) (void)hipHostFree(c->h_T);
   if (c->h_ticks) (void)hipHostFree(c->h_ticks);
+  if (c->h_order) (void)hipHostFree(c->h_order);
   if (c->h_k) (void)hipHostFree(c->h_k);
   if (c->h_err) (void)hipHostFree(c->h_err);
   if (c->pool) (void)hipFree(c->pool);
@@ -654,39 +659,47 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     if (dbw_status s = posted ? join_estimate(c) : estimate(c, t); s != DBW_OK) return s;
   }
   HostScope hq(c, DBW_KT_HOST_QUEUE);
-  // 2. this iteration's ticks into the pinned slot (its previous reader, the
-  //    choice of t-4, precedes the choice of t-2 the estimate waited for)
+  // 2. this iteration's ticks and arrival order (workers by (tick, index))
+  //    into the pinned slot (its previous reader, the PS kernel of t-4,
+  //    precedes the one of t-2 the estimate waited for)
   int64_t* hk = c->h_ticks + (size_t)slot * n;
   std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
+  int32_t* ho = c->h_order + (size_t)slot * n;
+  for (int i = 0; i < n; ++i) ho[i] = i;
+  std::stable_sort(ho, ho + n, [&](int32_t a, int32_t b) { return ticks_host[a] < ticks_host[b]; });
   std::vector<int64_t>& srt = c->sorted[slot];
-  srt.assign(ticks_host, ticks_host + n);
-  std::sort(srt.begin(), srt.end());
-  // 3. choose k_t and select the first k_t arrivals; the kernel reads T_hat
-  //    and the ticks from the pinned slot, keeps device copies, and writes
-  //    k_t back into the pinned slot
+  srt.resize(n);
+  for (int r = 0; r < n; ++r) srt[r] = ticks_host[ho[r]];
+  // 3. one PS kernel: the choice of k_t (T_hat read from the pinned slot, k_t
+  //    written back into it), the first k_t arrivals, the aggregate and the
+  //    update; then the statistics and the estimator bookkeeping (all on the
+  //    context stream: the gradient kernel fills every CU, so nothing would
+  //    run beside it)
   {
-    ProfScope ps(c, DBW_KT_CHOOSE);
+    ProfScope ps(c, DBW_KT_AGGREGATE);
     dbw::ChooseArgs ca{};
     ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
+    ca.order_src = c->d_order + (size_t)slot * n;
     ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.k_host = c->d_k + slot; ca.n = n; ca.eta = c->cfg.eta;
     ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
-    HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
-  }
-  HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
-  // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored
-  // above, and k_{t-1}); the rest of the queueing overlaps its solve
-  c->t = t + 1;
-  post_estimate(c, t + 1);
-  // 4. aggregate and update, then the statistics and the estimator
-  //    bookkeeping (all on the context stream: the gradient kernel fills
-  //    every CU, so nothing would run beside it)
-  {
-    ProfScope ps(c, DBW_KT_AGGREGATE);
     dbw::AggArgs aa{};
     aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;
     aa.eta = static_cast<float>(c->cfg.eta); aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_FUSED;
-    HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+    // every block of the fused kernel repeats the choice; beyond about two
+    // blocks per CU the separate choice kernel is cheaper
+    const bool fused = c->agg_nblocks <= dbw::kStepPsMaxBlocks;
+    if (fused) {
+      HIP_TRY(c, dbw::launch_step_ps(ca, aa, c->stream));
+    } else {
+      HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+    }
+    HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
+    if (!fused) HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
+    // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored
+    // above, and k_{t-1}); the rest of the queueing overlaps its solve
+    c->t = t + 1;
+    post_estimate(c, t + 1);
     dbw::FinalizeArgs fa{};
     fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = c->mask; fa.k_dev = c->k;
     fa.loss = loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;

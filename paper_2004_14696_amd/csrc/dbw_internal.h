@@ -94,6 +94,7 @@ struct ChooseArgs {
   const dbw_estimator_state* st;  // device
   const double* T_src;            // [n] time estimates (device or pinned host)
   const int64_t* ticks_src;       // [n] ticks (device or pinned host)
+  const int32_t* order_src;       // [n] workers by (tick, index) (pinned host; k_step_ps only)
   double* T_hat;                  // nullable device copy of T_src
   int64_t* ticks;                 // nullable device copy of ticks_src
   int32_t* k_host;                // nullable pinned host copy of k
@@ -127,6 +128,11 @@ struct AggArgs {
   int mode;
 };
 hipError_t launch_aggregate(const AggArgs& a, hipStream_t s);
+// Choice, selection by the host-sorted arrival order, and fused aggregation
+// in one launch (dbw_step); ca.order_src must be set.  Used up to this many
+// column tiles (about two blocks per CU).
+constexpr int64_t kStepPsMaxBlocks = 512;
+hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, hipStream_t s);
 
 struct FinalizeArgs {
   const float* sqpart;  // [n][nblocks]

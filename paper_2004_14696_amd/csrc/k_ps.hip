@@ -8,6 +8,9 @@
 //                   (Eq. grad_bw), per-column sums of squared deviations for
 //                   the variance estimate (Eq. sumvariancekt), per-row squared
 //                   norms, and optionally the SGD update (Eq. update).
+//  k_step_ps        the two above fused for dbw_step: every block repeats the
+//                   choice, the selection comes from the arrival order the
+//                   host sorted, and each block aggregates its column tile.
 //  k_finalize       reduces the per-block partials in a fixed order: the
 //                   iteration statistics (Eqs. sumvariancekt, normsquarekt,
 //                   loss estimate), per-worker squared norms, and the
@@ -26,6 +29,9 @@ namespace dbw {
 namespace {
 
 constexpr int WAVE = 64;
+// waves of a k_step_ps block: with few column tiles, each wave then has at
+// most one round of row loads for k <= 64
+constexpr int STEP_PS_WAVES = 16;
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -39,16 +45,47 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
-// Fixed-order block sum of doubles (blockDim.x == 256); result in all threads.
-__device__ double block_sum_256(double v, double* sh /*[4]*/) {
-  v = wave_sum_d(v);
-  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+// Lane exchange within rows of 16 lanes (xor 1, xor 2, half-row mirror, row
+// mirror): a butterfly whose four steps leave a row's combination in every
+// lane of the row.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const int lo = dpp_i<CTRL>(static_cast<int>(static_cast<uint32_t>(b)));
+  const int hi = dpp_i<CTRL>(static_cast<int>(static_cast<uint32_t>(b >> 32)));
+  return __builtin_bit_cast(double, (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) |
+                                        static_cast<uint32_t>(lo));
+}
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b)), l);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b >> 32)), l);
+  return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Fixed-order sums of doubles over the block (blockDim.x a multiple of 64,
+// at most 1024), M at a time; the results in all threads.
+template <int M>
+__device__ void block_sums_d(double (&v)[M], double* sh /*[16 M]*/) {
+#pragma unroll
+  for (int m = 0; m < M; ++m) v[m] = wave_sum_d(v[m]);
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, nw = blockDim.x / WAVE;
   __syncthreads();
-  if (l == 0) sh[w] = v;
+  if (l == 0)
+#pragma unroll
+    for (int m = 0; m < M; ++m) sh[m * 16 + w] = v[m];
   __syncthreads();
-  double r = ((sh[0] + sh[1]) + sh[2]) + sh[3];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    double r = sh[m * 16];
+    for (int i = 1; i < nw; ++i) r += sh[m * 16 + i];
+    v[m] = r;
+  }
   __syncthreads();
-  return r;
 }
 
 // Cooperative copy of the estimator state into LDS (whole 4-byte words).
@@ -74,30 +111,96 @@ __device__ __forceinline__ void better(double& r, int& k, double r2, int k2) {
   }
 }
 
+// LDS of the choice of k.
+struct ChooseShared {
+  dbw_estimator_state st;
+  double T[DBW_MAX_N];
+  int kfinal;
+};
+
+// The DBW choice of k_t from the staged state and T_hat (called by every
+// thread; wave 0 computes, k in sh.kfinal afterwards).  write: this block
+// stores k, b, the objective and the pinned copy of k.
+__device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
+#pragma clang fp contract(off)
+  const int tid = threadIdx.x, lane = tid % WAVE;
+  const int n = a.n;
+  const dbw_estimator_state& st = sh.st;
+  if (tid < WAVE) {
+    // D-window means (oldest first, summed in order as the definition
+    // reads), the same sequence in every lane
+    double V = 0.0, N = 0.0, L = 0.0;
+    for (int i = 0; i < st.nV; ++i) V += st.hV[i];
+    for (int i = 0; i < st.nV; ++i) N += st.hN[i];
+    for (int i = 0; i < st.nL; ++i) L += st.hL[i];
+    V = st.nV > 0 ? V / st.nV : 0.0;
+    N = st.nV > 0 ? N / st.nV : 0.0;
+    L = st.nL > 0 ? L / st.nL : 0.0;
+    const bool hasL = st.nL > 0;
+    const double ga = a.eta - L * a.eta * a.eta / 2.0;
+    const double gb = L * a.eta * a.eta / 2.0;
+    double best_r = -INFINITY;
+    int best_k = 0;
+    double maxG = -INFINITY;
+    for (int k = lane + 1; k <= n; k += WAVE) {
+      const double Gk = ga * N - gb * V / k;
+      const double T = sh.T[k - 1];
+      const bool eligible = isfinite(T) && T > 0.0;
+      const double r = eligible ? Gk / T : NAN;
+      if (write && a.objective) a.objective[k - 1] = hasL ? r : NAN;
+      maxG = fmax(maxG, Gk);
+      if (eligible) better(best_r, best_k, r, k);
+    }
+    // the best (objective, k) and the largest gain: within rows of 16 lanes,
+    // then over the four rows (both selections are exact)
+#define DBW_CHOOSE_STEP(CTRL)                                   \
+    better(best_r, best_k, dpp_d<CTRL>(best_r), dpp_i<CTRL>(best_k)); \
+    maxG = fmax(maxG, dpp_d<CTRL>(maxG));
+    DBW_CHOOSE_STEP(0xB1)
+    DBW_CHOOSE_STEP(0x4E)
+    DBW_CHOOSE_STEP(0x141)
+    DBW_CHOOSE_STEP(0x140)
+#undef DBW_CHOOSE_STEP
+    double r = readlane_d(best_r, 0), g = readlane_d(maxG, 0);
+    int kb = __builtin_amdgcn_readlane(best_k, 0);
+    for (int row = 1; row < 4; ++row) {
+      better(r, kb, readlane_d(best_r, 16 * row), __builtin_amdgcn_readlane(best_k, 16 * row));
+      g = fmax(g, readlane_d(maxG, 16 * row));
+    }
+    if (lane == 0) {
+      int k = (!hasL || kb == 0 || g < 0.0) ? n : kb;
+      // loss guard: never decrease k while the loss estimate rises
+      if (st.nF >= 2 && st.F_prev > a.beta * st.F_prev2 && st.k_prev < n) k = max(k, st.k_prev + 1);
+      if (write) {
+        a.k_out[0] = k;
+        a.b_out[0] = n - k;
+        if (a.k_host) *a.k_host = k;
+      }
+      sh.kfinal = k;
+    }
+  }
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
-#pragma clang fp contract(off)
-  __shared__ dbw_estimator_state st;
-  __shared__ double sh_T[DBW_MAX_N];
+  __shared__ ChooseShared sh;
   __shared__ long long sh_t[DBW_MAX_N];
-  __shared__ double sh_r[4], sh_g[4], sh_win[3];
-  __shared__ int sh_k[4], sh_cnt[4];
-  __shared__ int sh_kfinal;
+  __shared__ int sh_cnt[16];
   const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
   const int n = a.n;
 
-  // stage the inputs (T_hat and ticks may live in pinned host memory)
-  if (a.do_choose) {
-    load_state(a.st, &st);
-    for (int k = tid; k < n; k += blockDim.x) {
-      const double T = a.T_src[k];
-      sh_T[k] = T;
-      if (a.T_hat) a.T_hat[k] = T;
+  // stage the inputs (T_hat and ticks may live in pinned host memory); all
+  // loads are issued before their values are used
+  if (a.do_choose) load_state(a.st, &sh.st);
+  for (int i = tid; i < n; i += blockDim.x) {
+    const double T = a.do_choose ? a.T_src[i] : 0.0;
+    const long long t = a.do_select ? a.ticks_src[i] : 0;
+    if (a.do_choose) {
+      sh.T[i] = T;
+      if (a.T_hat) a.T_hat[i] = T;
     }
-  }
-  if (a.do_select) {
-    for (int i = tid; i < n; i += blockDim.x) {
-      const long long t = a.ticks_src[i];
+    if (a.do_select) {
       sh_t[i] = t;
       if (a.ticks) a.ticks[i] = t;
     }
@@ -105,66 +208,14 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
   __syncthreads();
 
   if (a.do_choose) {
-    // D-window means (oldest first, summed in order as the definition reads)
-    if (tid == 0) {
-      double V = 0.0, N = 0.0, L = 0.0;
-      for (int i = 0; i < st.nV; ++i) V += st.hV[i];
-      for (int i = 0; i < st.nV; ++i) N += st.hN[i];
-      for (int i = 0; i < st.nL; ++i) L += st.hL[i];
-      sh_win[0] = st.nV > 0 ? V / st.nV : 0.0;
-      sh_win[1] = st.nV > 0 ? N / st.nV : 0.0;
-      sh_win[2] = st.nL > 0 ? L / st.nL : 0.0;
-    }
+    choose_k(a, sh, true);
+  } else {
+    if (tid == 0) sh.kfinal = a.k_imm;
     __syncthreads();
-    const bool hasL = st.nL > 0;
-    const double V = sh_win[0], N = sh_win[1], L = sh_win[2];
-    const double ga = a.eta - L * a.eta * a.eta / 2.0;
-    const double gb = L * a.eta * a.eta / 2.0;
-    double best_r = -INFINITY;
-    int best_k = 0;
-    double maxG = -INFINITY;
-    for (int k = tid + 1; k <= n; k += blockDim.x) {
-      const double Gk = ga * N - gb * V / k;
-      const double T = sh_T[k - 1];
-      const bool eligible = isfinite(T) && T > 0.0;
-      const double r = eligible ? Gk / T : NAN;
-      if (a.objective) a.objective[k - 1] = hasL ? r : NAN;
-      maxG = fmax(maxG, Gk);
-      if (eligible) better(best_r, best_k, r, k);
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      better(best_r, best_k, __shfl_xor(best_r, o, WAVE), __shfl_xor(best_k, o, WAVE));
-      maxG = fmax(maxG, __shfl_xor(maxG, o, WAVE));
-    }
-    if (lane == 0) {
-      sh_r[wv] = best_r;
-      sh_k[wv] = best_k;
-      sh_g[wv] = maxG;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      double r = sh_r[0], g = sh_g[0];
-      int kb = sh_k[0];
-      for (int w = 1; w < 4; ++w) {
-        better(r, kb, sh_r[w], sh_k[w]);
-        g = fmax(g, sh_g[w]);
-      }
-      int k = (!hasL || kb == 0 || g < 0.0) ? n : kb;
-      // loss guard: never decrease k while the loss estimate rises
-      if (st.nF >= 2 && st.F_prev > a.beta * st.F_prev2 && st.k_prev < n) k = max(k, st.k_prev + 1);
-      a.k_out[0] = k;
-      a.b_out[0] = n - k;
-      if (a.k_host) *a.k_host = k;
-      sh_kfinal = k;
-    }
-  } else if (tid == 0) {
-    sh_kfinal = a.k_imm;
   }
-  __syncthreads();
 
   if (a.do_select) {
-    const int k = sh_kfinal;
+    const int k = sh.kfinal;
     int finite = 0;
     for (int i = tid; i < n; i += blockDim.x) {
       const long long ti = sh_t[i];
@@ -182,7 +233,11 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
     for (int o = 32; o > 0; o >>= 1) finite += __shfl_xor(finite, o, WAVE);
     if (lane == 0) sh_cnt[wv] = finite;
     __syncthreads();
-    if (tid == 0 && k > sh_cnt[0] + sh_cnt[1] + sh_cnt[2] + sh_cnt[3]) atomicOr(a.err, ERR_K_RANGE);
+    if (tid == 0) {
+      int total = 0;
+      for (int w = 0; w < static_cast<int>(blockDim.x / WAVE); ++w) total += sh_cnt[w];
+      if (k > total) atomicOr(a.err, ERR_K_RANGE);
+    }
   }
 }
 
@@ -221,72 +276,87 @@ __device__ __forceinline__ int col_index(int lane, int q) {
   return VEC4 ? lane * 4 + q : lane + WAVE * q;
 }
 
-template <bool VEC4, int MODE>
-__global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
-  __shared__ float sh_s1[AGG_WAVES][AGG_TILE];
-  __shared__ float sh_s2[AGG_WAVES][AGG_TILE];
-  __shared__ float sh_c[AGG_TILE];
-  __shared__ double sh_red[4];
+// LDS of one aggregation tile worked by NW waves.
+template <int NW>
+struct AggShared {
+  float s1[NW][AGG_TILE];
+  float s2[NW][AGG_TILE];
+  float c[AGG_TILE];
+  double red[32];
+};
+
+// Pieces of one block's column tile of the aggregation over the rows listed
+// in sel (generic pointer: global or LDS).  The block's NW waves split the
+// rows, AGG_U rows in flight per wave; the first AGG_TILE threads finish the
+// columns.
+constexpr int AGG_U = 4;
+
+// Loads of rows r0 + u NW (u < AGG_U) below rmax; jj = -1 past rmax.
+template <bool VEC4, int NW>
+__device__ __forceinline__ void agg_load_round(const AggArgs& a, const int32_t* sel, int r0, int rmax,
+                                               float (&x)[AGG_U][4], int (&jj)[AGG_U]) {
+  const int lane = threadIdx.x % WAVE;
+  const int64_t base = (int64_t)blockIdx.x * AGG_TILE;
+#pragma unroll
+  for (int u = 0; u < AGG_U; ++u) {
+    const int r = r0 + u * NW;
+    jj[u] = r < rmax ? __builtin_amdgcn_readfirstlane(sel[r]) : -1;   // uniform per wave
+    load_tile<VEC4>(a.G + (int64_t)(jj[u] < 0 ? 0 : jj[u]) * a.P, base, lane, a.P, x[u], jj[u] >= 0);
+  }
+}
+
+// Shifted sums of the loaded rows, and their squared norms.
+template <int MODE>
+__device__ __forceinline__ void agg_accumulate(const AggArgs& a, const float (&x)[AGG_U][4], const int (&jj)[AGG_U],
+                                               const float (&c)[4], float (&s1)[4], float (&s2)[4]) {
+  const int lane = threadIdx.x % WAVE;
+#pragma unroll
+  for (int u = 0; u < AGG_U; ++u) {
+    if (jj[u] < 0) break;
+    float sq = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float dv = x[u][q] - c[q];
+      s1[q] += dv;
+      s2[q] = fmaf(dv, dv, s2[q]);
+      sq = fmaf(x[u][q], x[u][q], sq);
+    }
+    if (MODE != AGG_MEAN) {
+      sq = wave_sum(sq);
+      if (lane == 0) a.sqpart[(int64_t)jj[u] * gridDim.x + blockIdx.x] = sq;
+    }
+  }
+}
+
+// Column results from the waves' partial sums: g, the update, and the block
+// partials of the statistics.
+template <bool VEC4, int MODE, int NW>
+__device__ void agg_finish(const AggArgs& a, int k, const float (&c)[4], const float (&s1)[4], const float (&s2)[4],
+                           AggShared<NW>& sh, const float* w_old = nullptr) {
   const int tid = threadIdx.x;
   const int lane = tid % WAVE, wv = tid / WAVE;
   const int64_t P = a.P;
   const int64_t blk = blockIdx.x;
-  const int64_t nblocks = gridDim.x;
   const int64_t base = blk * AGG_TILE;
-  const int k = a.k_dev ? a.k_dev[0] : a.k_imm;
-
-  // shift: the mean itself (given) or the fastest worker's row
-  float c[4];
-  if (MODE == AGG_STATS_GIVEN_MEAN) load_tile<VEC4>(a.g_in, base, lane, P, c);
-  else load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(a.sel[0]) * P, base, lane, P, c);
-
-  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
-  constexpr int U = 4;   // rows in flight per wave
-  for (int r0 = wv; r0 < k; r0 += AGG_WAVES * U) {
-    float x[U][4];
-    int jj[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = r0 + u * AGG_WAVES;
-      jj[u] = r < k ? __builtin_amdgcn_readfirstlane(a.sel[r]) : -1;   // uniform per wave
-      load_tile<VEC4>(a.G + (int64_t)(jj[u] < 0 ? 0 : jj[u]) * P, base, lane, P, x[u], jj[u] >= 0);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (jj[u] < 0) break;
-      float sq = 0.f;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float dv = x[u][q] - c[q];
-        s1[q] += dv;
-        s2[q] = fmaf(dv, dv, s2[q]);
-        sq = fmaf(x[u][q], x[u][q], sq);
-      }
-      if (MODE != AGG_MEAN) {
-        sq = wave_sum(sq);
-        if (lane == 0) a.sqpart[(int64_t)jj[u] * nblocks + blk] = sq;
-      }
-    }
-  }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    sh_s1[wv][col_index<VEC4>(lane, q)] = s1[q];
-    sh_s2[wv][col_index<VEC4>(lane, q)] = s2[q];
-    if (wv == 0) sh_c[col_index<VEC4>(lane, q)] = c[q];
+    sh.s1[wv][col_index<VEC4>(lane, q)] = s1[q];
+    sh.s2[wv][col_index<VEC4>(lane, q)] = s2[q];
+    if (wv == 0) sh.c[col_index<VEC4>(lane, q)] = c[q];
   }
   __syncthreads();
 
   const int64_t col = base + tid;
   const float kf = static_cast<float>(k);
-  float S1 = 0.f, S2 = 0.f;
-#pragma unroll
-  for (int w = 0; w < AGG_WAVES; ++w) {
-    S1 += sh_s1[w][tid];
-    S2 += sh_s2[w][tid];
-  }
   double m2 = 0.0, g2 = 0.0;
-  if (col < P) {
-    const float cs = sh_c[tid];
+  if (tid < AGG_TILE && col < P) {
+    float S1 = 0.f, S2 = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      S1 += sh.s1[w][tid];
+      S2 += sh.s2[w][tid];
+    }
+    const float cs = sh.c[tid];
     float g;
     if (MODE == AGG_STATS_GIVEN_MEAN) {
       g = cs;
@@ -296,19 +366,124 @@ __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
       a.g_out[col] = g;
       if (MODE == AGG_FUSED) {
         m2 = S2 - S1 * S1 / kf;
-        if (a.w) a.w[col] = a.w[col] - a.eta * g;
+        if (a.w) a.w[col] = (w_old ? *w_old : a.w[col]) - a.eta * g;
       }
     }
     g2 = static_cast<double>(g) * g;
   }
   if (MODE != AGG_MEAN) {
-    m2 = block_sum_256(m2, sh_red);
-    g2 = block_sum_256(g2, sh_red);
+    double v[2] = {m2, g2};
+    block_sums_d<2>(v, sh.red);
     if (tid == 0) {
-      a.part[blk * 2 + 0] = m2;
-      a.part[blk * 2 + 1] = g2;
+      a.part[blk * 2 + 0] = v[0];
+      a.part[blk * 2 + 1] = v[1];
     }
   }
+}
+
+// The shift row's tile: the mean itself (given) or the fastest worker's row.
+template <bool VEC4, int MODE>
+__device__ __forceinline__ void agg_shift(const AggArgs& a, const int32_t* sel, float (&c)[4]) {
+  const int lane = threadIdx.x % WAVE;
+  const int64_t base = (int64_t)blockIdx.x * AGG_TILE;
+  if (MODE == AGG_STATS_GIVEN_MEAN) load_tile<VEC4>(a.g_in, base, lane, a.P, c);
+  else load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(sel[0]) * a.P, base, lane, a.P, c);
+}
+
+template <bool VEC4, int MODE, int NW>
+__device__ void aggregate_tile(const AggArgs& a, const int32_t* sel, int k, AggShared<NW>& sh) {
+  const int wv = threadIdx.x / WAVE;
+  float c[4];
+  agg_shift<VEC4, MODE>(a, sel, c);
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int r0 = wv; r0 < k; r0 += NW * AGG_U) {
+    float x[AGG_U][4];
+    int jj[AGG_U];
+    agg_load_round<VEC4, NW>(a, sel, r0, k, x, jj);
+    agg_accumulate<MODE>(a, x, jj, c, s1, s2);
+  }
+  agg_finish<VEC4, MODE, NW>(a, k, c, s1, s2, sh);
+}
+
+template <bool VEC4, int MODE>
+__global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
+  __shared__ AggShared<AGG_WAVES> sh;
+  const int k = a.k_dev ? a.k_dev[0] : a.k_imm;
+  aggregate_tile<VEC4, MODE, AGG_WAVES>(a, a.sel, k, sh);
+}
+
+// The PS side of one DBW iteration in one launch: every block makes the
+// choice of k_t itself (the same fp64 arithmetic on the same staged inputs,
+// so every block reaches the same k), takes the first k_t workers of the
+// arrival order the host sorted (ties to the lower index), and aggregates its
+// column tile with the SGD update; block 0 also stores the choice, the
+// selection and the device copies of T_hat and the ticks.
+template <bool VEC4>
+__global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca, AggArgs a) {
+  constexpr int NW = STEP_PS_WAVES;
+  __shared__ ChooseShared cs;
+  __shared__ AggShared<NW> sh;
+  __shared__ int32_t sh_order[DBW_MAX_N];
+  __shared__ long long sh_t[DBW_MAX_N];
+  __shared__ int sh_cnt[16];
+  const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
+  const int n = ca.n;
+  const bool lead = blockIdx.x == 0;
+  // every host and device read of the prologue is issued before any use
+  load_state(ca.st, &cs.st);
+  const int64_t col = (int64_t)blockIdx.x * AGG_TILE + tid;
+  const float w_old = tid < AGG_TILE && col < a.P && a.w ? a.w[col] : 0.f;
+  for (int i = tid; i < n; i += blockDim.x) {
+    const double T = ca.T_src[i];
+    const int32_t o = ca.order_src[i];
+    const long long t = lead ? ca.ticks_src[i] : 0;
+    cs.T[i] = T;
+    sh_order[i] = o;
+    if (lead) {
+      sh_t[i] = t;
+      if (ca.T_hat) ca.T_hat[i] = T;
+      if (ca.ticks) ca.ticks[i] = t;
+    }
+  }
+  __syncthreads();
+  // the first rows of the arrival order are loaded while the choice runs
+  // (k_t >= 1 rows are needed; rows past k_t are dropped)
+  float c[4];
+  agg_shift<VEC4, AGG_FUSED>(a, sh_order, c);
+  float x[AGG_U][4];
+  int jj[AGG_U];
+  agg_load_round<VEC4, NW>(a, sh_order, wv, n, x, jj);
+  choose_k(ca, cs, lead);
+  const int k = cs.kfinal;
+  if (lead) {
+    int finite = 0;
+    for (int r = tid; r < n; r += blockDim.x) {
+      const int i = sh_order[r];
+      const long long t = sh_t[i];
+      ca.mask[i] = r < k ? 1 : 0;
+      if (r < k) ca.sel[r] = i;
+      finite += t < INT64_MAX;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) finite += __shfl_xor(finite, o, WAVE);
+    if (lane == 0) sh_cnt[wv] = finite;
+    __syncthreads();
+    if (tid == 0) {
+      int total = 0;
+      for (int w = 0; w < NW; ++w) total += sh_cnt[w];
+      if (k > total) atomicOr(ca.err, ERR_K_RANGE);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < AGG_U; ++u)
+    if (wv + u * NW >= k) jj[u] = -1;
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+  agg_accumulate<AGG_FUSED>(a, x, jj, c, s1, s2);
+  for (int r0 = wv + NW * AGG_U; r0 < k; r0 += NW * AGG_U) {
+    agg_load_round<VEC4, NW>(a, sh_order, r0, k, x, jj);
+    agg_accumulate<AGG_FUSED>(a, x, jj, c, s1, s2);
+  }
+  agg_finish<VEC4, AGG_FUSED, NW>(a, k, c, s1, s2, sh, &w_old);
 }
 
 // ---------------------------------------------------------------------------
@@ -324,7 +499,7 @@ __device__ void push_window(double* h, int32_t* cnt, int D, double v) {
 
 __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
 #pragma clang fp contract(off)
-  __shared__ double sh_red[4];
+  __shared__ double sh_red[64];
   const int tid = threadIdx.x;
   const int k = a.k_dev ? a.k_dev[0] : a.k_imm;
   if (blockIdx.x > 0) {
@@ -356,10 +531,14 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
       ls += static_cast<double>(a.loss[j]);
       cnt += 1.0;
     }
-  m2 = block_sum_256(m2, sh_red);
-  g2 = block_sum_256(g2, sh_red);
-  ls = block_sum_256(ls, sh_red);
-  cnt = block_sum_256(cnt, sh_red);
+  {
+    double v[4] = {m2, g2, ls, cnt};
+    block_sums_d<4>(v, sh_red);
+    m2 = v[0];
+    g2 = v[1];
+    ls = v[2];
+    cnt = v[3];
+  }
   if (tid == 0) {
     if (static_cast<int>(cnt) != k) atomicOr(a.err, ERR_MASK_COUNT);
     double V_plus;
@@ -432,6 +611,14 @@ hipError_t launch_aggregate(const AggArgs& a, hipStream_t s) {
     else DBW_AGG_LAUNCH(false, AGG_FUSED);
   }
 #undef DBW_AGG_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
+  const dim3 block(STEP_PS_WAVES * WAVE);
+  if ((a.P % 4) == 0) hipLaunchKernelGGL(k_step_ps<true>, grid, block, 0, s, ca, a);
+  else hipLaunchKernelGGL(k_step_ps<false>, grid, block, 0, s, ca, a);
   return hipGetLastError();
 }
 
