@@ -70,6 +70,8 @@ class DBWConfig:
     times: TimeModel = field(default_factory=TimeModel)
     seed: int = 14696           # base of the seed sequence
     labels: str = "uniform"     # "uniform" or "teacher" (test fixture)
+    clock: str = "fresh"        # "fresh": every worker starts each iteration afresh;
+                                # "psw": Push & Wait, late workers finish their current gradient first
 
     @property
     def param_count(self) -> int:

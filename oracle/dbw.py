@@ -16,9 +16,11 @@ End of iteration t (Sect. 3.1, Sect. 3.2):
   * for t >= 1, L+_t = 2 (eta N+_{t-1} - (F_hat_{t-1} - F_hat_t))
                      / (eta^2 (N+_{t-1} + V+_{t-1} / k_{t-1}))      (Eq. estimateL)
     is pushed when the denominator is positive;
-  * all n arrival-ordered ticks of iteration t are recorded as samples of
-    row h = k_{t-1} (late workers still notify completion);
-  * the virtual clock advances by the k_t-th smallest tick.
+  * the arrival offsets of iteration t (from the round-trip ticks, through the
+    clock of the configuration: fresh start or Push & Wait, oracle/clock.py)
+    of the workers that computed w_t are recorded, in arrival order, as
+    samples of row h = k_{t-1} (late workers still notify completion);
+  * the virtual clock advances by the k_t-th smallest offset.
 
 Test infrastructure only (see the package docstring).
 """
@@ -27,6 +29,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import model, ps
+from .clock import make_clock
 from .time_estimator import time_estimate
 
 
@@ -93,6 +96,7 @@ class DBWOracle:
         self.t = 0
         self.cnt = [[0] * n for _ in range(n)]
         self.tsum = [[0] * n for _ in range(n)]
+        self.vclock = make_clock(getattr(cfg, "clock", "fresh"), n)
         self.clock = 0
 
     # -- pieces ------------------------------------------------------------
@@ -106,14 +110,16 @@ class DBWOracle:
         return choose_k(c.n, c.eta, c.beta, c.D, self.hV, self.hN, self.hL, self.F,
                         self.k_prev, T_hat)
 
-    def record_times(self, ticks, k_t):
-        """Bookkeeping of the arrival times of this iteration (row k_{t-1})."""
-        srt = sorted(int(x) for x in ticks)
+    def record_times(self, offsets, k_t):
+        """Bookkeeping of the arrival offsets of this iteration (row k_{t-1}):
+        the samples of the workers that computed w_t, and the clock."""
+        samples, computed = self.vclock.advance(offsets, k_t)
         h = self.k_prev
-        for i, v in enumerate(srt):
+        for i, v in enumerate(samples):
             self.cnt[h - 1][i] += 1
             self.tsum[h - 1][i] += v
-        self.clock += srt[k_t - 1]
+        self.clock = self.vclock.s
+        return computed
 
     # -- the iteration -------------------------------------------------------
     def step(self, Xt, yt, ticks, T_hat=None, k_force=None):
@@ -121,6 +127,7 @@ class DBWOracle:
         round-trip ticks [n].  ``T_hat`` overrides the time estimate and
         ``k_force`` the choice (static-k runs, lockstep tests)."""
         c = self.cfg
+        offsets = self.vclock.offsets(ticks)
         if T_hat is None:
             T_hat = self.time_estimate()
         k_t, objective = self.choose(T_hat)
@@ -128,7 +135,7 @@ class DBWOracle:
             k_t = int(k_force)
         V_window = window_mean(self.hV, c.D)
         G, loss = model.worker_grads(c, self.w, Xt, yt)
-        sel, mask = ps.select_fastest(ticks, k_t)
+        sel, mask = ps.select_fastest(offsets, k_t)
         g = ps.aggregate(G, sel)
         st = ps.grad_stats(G, sel, g, loss, V_window if V_window is not None else 0.0)
         w_next = ps.sgd_update(self.w, g, c.eta)
@@ -142,8 +149,9 @@ class DBWOracle:
         self.F.append(st["F_hat"])
         if L_new is not None:
             self.hL.append(L_new)
-        self.record_times(ticks, k_t)
+        computed = self.record_times(offsets, k_t)
         rec = {"t": self.t, "k": k_t, "b": c.n - k_t, "objective": objective,
+               "offsets": offsets, "computed": computed,
                "T_hat": T_hat, "G": G, "loss": loss, "sel": sel, "mask": mask, "g": g,
                "w_prev": self.w, "w": w_next, "L_plus": L_new, **st}
         self.w = w_next
