@@ -130,6 +130,8 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C3")
+    ap.add_argument("--clock", choices=("fresh", "psw"), default="fresh",
+                    help="virtual clock: every worker starts each iteration afresh, or Push & Wait")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true",
@@ -150,6 +152,8 @@ def main(argv=None) -> int:
     from dbw_inputs import generate as gen
 
     cfg = get(args.workload)
+    if args.clock != cfg.clock:
+        cfg = cfg.replace(clock=args.clock)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     if args.traffic_probe:
@@ -256,7 +260,7 @@ def main(argv=None) -> int:
                         f"C={cfg.C}, minibatches gathered by index from a resident {cfg.S}x{cfg.d} dataset"
             if cfg.model == "softmax" else
             f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows",
-            "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P,
+            "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P, "clock": cfg.clock,
         },
         "roofline": {
             "kernel": "worker gradients (dbw_worker_grads)",

@@ -53,20 +53,32 @@ typedef enum {
 
 typedef enum { DBW_SOFTMAX = 0, DBW_MLP = 1 } dbw_model;
 
+/* Virtual clock of the simulated cluster (Sect. 2, the synchronisation
+ * variants; Sect. 3.2).  FRESH: every worker starts each iteration at its
+ * beginning, so a worker's arrival offset is its round-trip time and all n
+ * arrivals are samples.  PSW (Push & Wait): the PS pushes w_{t+1} once it
+ * holds k_t gradients of w_t; a worker still computing a gradient of an older
+ * vector finishes it, then takes the most recent vector; with s_t the start
+ * of iteration t and b_i the time worker i becomes free, worker i computes
+ * w_t iff b_i <= s_t or b_i < s_{t+1}, its offset is
+ * max(s_t, b_i) - s_t + tau_i, and a worker still busy at s_{t+1} skips w_t
+ * (no sample: the estimate's data are censored). */
+typedef enum { DBW_CLOCK_FRESH = 0, DBW_CLOCK_PSW = 1 } dbw_clock;
+
 #define DBW_MAX_N 1024 /* logical workers per context                       */
 #define DBW_MAX_D 64   /* length of the estimator averaging window D          */
 
 /* Problem description.  n workers, minibatch B per worker, d input features,
  * C classes, H hidden units (MLP only), learning rate eta (constant for all
  * k), window D of the estimator averages, loss guard factor beta >= 1
- * (Eq. greedy2).  S > 0 declares a resident dataset of S rows that minibatches
- * may index (see dbw_worker_grads); S = 0 means minibatches are passed
- * materialised. */
+ * (Eq. greedy2), virtual clock (dbw_clock; 0 = fresh start).  S > 0 declares
+ * a resident dataset of S rows that minibatches may index (see
+ * dbw_worker_grads); S = 0 means minibatches are passed materialised. */
 typedef struct {
   int32_t model; /* dbw_model */
   int32_t n, B, d, C, H;
   int32_t D;
-  int32_t reserved0;
+  int32_t clock; /* dbw_clock */
   double eta, beta;
   int64_t S;
 } dbw_config;
@@ -161,12 +173,16 @@ dbw_status dbw_choose_b(dbw_ctx* ctx, const double* T_hat, int32_t* k_out, int32
  * far (host, Eq. quadratic_opt), choose k_t, compute all n worker gradients,
  * aggregate the k_t first arrivals, compute the statistics, update
  * w <- w - eta g_t (w DEVICE float [P], 16-byte aligned, in place), and push the estimator
- * state.  X, y, rows as in dbw_worker_grads.  ticks_host (HOST int64 [n]) are
- * this iteration's round-trip ticks; they are recorded as samples of row
- * h = k_{t-1} once k_{t-1} is known, and advance the virtual clock by the
- * k_t-th smallest tick.  If k_host is not NULL the call waits for the
- * iteration's choice and stores k_t there; otherwise it returns as soon as the
- * work is queued. */
+ * state.  X, y, rows as in dbw_worker_grads.  ticks_host (HOST int64 [n],
+ * >= 0) are the round-trip ticks tau_i of the gradient each worker computes
+ * next; the context's clock turns them into arrival offsets (equal to them
+ * under DBW_CLOCK_FRESH; under DBW_CLOCK_PSW the call first waits for k_{t-1}
+ * and the offsets must stay below 2^48).  The k_t smallest offsets (ties to
+ * the lower worker index) are aggregated; once k_t is known the offsets of
+ * the workers that compute w_t are recorded, in arrival order, as samples of
+ * row h = k_{t-1}, and the virtual clock advances by the k_t-th smallest
+ * offset.  If k_host is not NULL the call waits for the iteration's choice and
+ * stores k_t there; otherwise it returns as soon as the work is queued. */
 dbw_status dbw_step(dbw_ctx* ctx, float* w, const float* X, const int32_t* y,
                     const int32_t* rows, const int64_t* ticks_host, int32_t* k_host);
 
@@ -224,10 +240,18 @@ dbw_status dbw_state_import(dbw_ctx* ctx, const dbw_estimator_state* in);
 
 /* Arrival-time samples (HOST int64 [n][n] each, as in dbw_time_estimate) and
  * the virtual clock (HOST int64, ticks).  Export first folds in every
- * iteration whose row is known (it synchronises the stream). */
+ * iteration whose row is known (it synchronises the stream).  Import also
+ * marks every worker idle at the imported clock (DBW_CLOCK_PSW). */
 dbw_status dbw_samples_export(dbw_ctx* ctx, int64_t* cnt, int64_t* tsum, int64_t* clock);
 dbw_status dbw_samples_import(dbw_ctx* ctx, const int64_t* cnt, const int64_t* tsum,
                               int64_t clock);
+
+/* Push & Wait clock: the time each worker becomes free (HOST int64 [n],
+ * ticks on the virtual clock).  Export folds like dbw_samples_export; import
+ * replaces the times (each >= 0; DBW_EINVAL otherwise).  Resume and lockstep
+ * testing. */
+dbw_status dbw_busy_export(dbw_ctx* ctx, int64_t* busy);
+dbw_status dbw_busy_import(dbw_ctx* ctx, const int64_t* busy);
 
 /* Kernel timing with HIP events on the streams the kernels run on.  With
  * dbw_profile_enable(ctx, 1) every launch of the device groups is bracketed

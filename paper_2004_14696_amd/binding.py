@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libdbw.so")
 
 DBW_OK, DBW_EINVAL, DBW_ERANGE, DBW_EHIP, DBW_ESTATE, DBW_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 DBW_SOFTMAX, DBW_MLP = 0, 1
+DBW_CLOCK_FRESH, DBW_CLOCK_PSW = 0, 1
 DBW_MAX_N, DBW_MAX_D = 1024, 64
 DBW_KT_GRADS, DBW_KT_AGGREGATE, DBW_KT_CHOOSE, DBW_KT_HOST_ESTIMATE, DBW_KT_HOST_STEP = 0, 1, 2, 3, 4
 DBW_KT_HOST_WAIT, DBW_KT_HOST_QUEUE = 5, 6
@@ -32,7 +33,7 @@ EXPORTED = (
     "dbw_step_outputs", "dbw_time_estimate", "dbw_state_export", "dbw_state_import",
     "dbw_samples_export", "dbw_samples_import", "dbw_profile_enable", "dbw_kernel_time",
     "dbw_profile_reset", "dbw_time_estimator_create", "dbw_time_estimator_destroy",
-    "dbw_time_estimator_solve", "dbw_time_estimator_stats",
+    "dbw_time_estimator_solve", "dbw_time_estimator_stats", "dbw_busy_export", "dbw_busy_import",
 )
 
 
@@ -44,7 +45,7 @@ class DBWError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [("model", c_int32), ("n", c_int32), ("B", c_int32), ("d", c_int32),
-                ("C", c_int32), ("H", c_int32), ("D", c_int32), ("reserved0", c_int32),
+                ("C", c_int32), ("H", c_int32), ("D", c_int32), ("clock", c_int32),
                 ("eta", c_double), ("beta", c_double), ("S", c_int64)]
 
 
@@ -109,6 +110,10 @@ def load_library(path: str = LIB_PATH):
     lib.dbw_time_estimator_solve.restype = st
     lib.dbw_time_estimator_stats.argtypes = [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)]
     lib.dbw_time_estimator_stats.restype = st
+    lib.dbw_busy_export.argtypes = [P, POINTER(c_int64)]
+    lib.dbw_busy_export.restype = st
+    lib.dbw_busy_import.argtypes = [P, POINTER(c_int64)]
+    lib.dbw_busy_import.restype = st
     lib.dbw_state_export.argtypes = [P, POINTER(EstimatorState)]
     lib.dbw_state_export.restype = st
     lib.dbw_state_import.argtypes = [P, POINTER(EstimatorState)]
@@ -128,10 +133,12 @@ def load_library(path: str = LIB_PATH):
 
 
 def make_config(model: str | int, n: int, B: int, d: int, C: int, H: int = 0, eta: float = 0.1,
-                beta: float = 1.01, D: int = 5, S: int = 0) -> Config:
+                beta: float = 1.01, D: int = 5, S: int = 0, clock: str | int = DBW_CLOCK_FRESH) -> Config:
     if isinstance(model, str):
         model = {"softmax": DBW_SOFTMAX, "mlp": DBW_MLP}[model]
-    return Config(model=model, n=n, B=B, d=d, C=C, H=H, D=D, reserved0=0, eta=eta, beta=beta, S=S)
+    if isinstance(clock, str):
+        clock = {"fresh": DBW_CLOCK_FRESH, "psw": DBW_CLOCK_PSW}[clock]
+    return Config(model=model, n=n, B=B, d=d, C=C, H=H, D=D, clock=clock, eta=eta, beta=beta, S=S)
 
 
 def param_count(cfg: Config) -> int:
@@ -403,6 +410,18 @@ class Context:
                                                 tsum.ctypes.data_as(POINTER(c_int64)), ctypes.byref(clock)),
                     "dbw_samples_export")
         return cnt, tsum, int(clock.value)
+
+    def export_busy(self) -> np.ndarray:
+        """Push & Wait: the time each worker becomes free (ticks)."""
+        out = np.empty(self.cfg.n, dtype=np.int64)
+        self._check(self.lib.dbw_busy_export(self.h, out.ctypes.data_as(POINTER(c_int64))), "dbw_busy_export")
+        return out
+
+    def import_busy(self, busy):
+        b = np.ascontiguousarray(busy, dtype=np.int64)
+        if b.shape != (self.cfg.n,):
+            raise ValueError(f"busy must have shape ({self.cfg.n},)")
+        self._check(self.lib.dbw_busy_import(self.h, b.ctypes.data_as(POINTER(c_int64))), "dbw_busy_import")
 
     def import_samples(self, cnt, tsum, clock: int = 0):
         cnt = np.ascontiguousarray(cnt, dtype=np.int64)

@@ -100,9 +100,12 @@ struct dbw_ctx {
   int32_t k_prev_base = 0;      // k_{base-1}
   int64_t recorded = 0;         // iterations whose samples are in the grid
   int64_t clocked = 0;          // iterations whose k-th arrival advanced the clock
-  std::vector<int64_t> sorted[kSlots];
+  std::vector<int64_t> sorted[kSlots];  // arrival offsets of the slot's iteration, ascending
+  std::vector<int64_t> offs[kSlots];    // the same by worker (Push & Wait)
   std::vector<int64_t> cnt, tsum;
-  int64_t clock = 0;
+  int64_t clock = 0;                    // start of the next iteration to fold
+  std::vector<int64_t> busy;            // Push & Wait: time each worker becomes free
+  std::vector<int64_t> psw_samples;     // scratch
   std::vector<double> T_scratch;
   dbw::IsoSolver solver;
   std::vector<int> pending_rows;  // grid rows changed since the solver's last call
@@ -174,6 +177,7 @@ bool config_ok(const dbw_config* c, std::string* why) {
   else if (!(c->beta >= 1.0) || !std::isfinite(c->beta)) *why = "beta must be finite and >= 1";
   else if (c->S < 0 || c->S > (int64_t{1} << 31)) *why = "S outside [0, 2^31]";
   else if ((int64_t)c->n * c->B > (int64_t{1} << 30)) *why = "n*B too large";
+  else if (c->clock != DBW_CLOCK_FRESH && c->clock != DBW_CLOCK_PSW) *why = "clock must be DBW_CLOCK_FRESH or DBW_CLOCK_PSW";
   else return true;
   return false;
 }
@@ -206,9 +210,40 @@ dbw_status known_k(dbw_ctx* c, int64_t u, int32_t* k) {
 }
 
 // Fold into the grid every iteration u < upto whose row k_{u-1} is known, and
-// into the clock every iteration u < clock_upto.
+// into the clock every iteration u < clock_upto.  Under Push & Wait the
+// samples of iteration u depend on who computed w_u, which needs k_u and the
+// clock at u, so both advance together up to max(upto, clock_upto).
 dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
   const int n = c->cfg.n;
+  if (c->cfg.clock == DBW_CLOCK_PSW) {
+    const int64_t end = std::max(upto, clock_upto);
+    while (c->recorded < end) {
+      const int64_t u = c->recorded;
+      int32_t h, k;
+      dbw_status s = known_k(c, u - 1, &h);
+      if (s == DBW_OK) s = known_k(c, u, &k);
+      if (s != DBW_OK) return s;
+      const std::vector<int64_t>& o = c->offs[u % kSlots];
+      const int64_t s_next = c->clock + c->sorted[u % kSlots][k - 1];
+      std::vector<int64_t>& smp = c->psw_samples;
+      smp.clear();
+      for (int i = 0; i < n; ++i)
+        if (c->busy[i] <= c->clock || c->busy[i] < s_next) {   // computed w_u
+          smp.push_back(o[i]);
+          c->busy[i] = c->clock + o[i];
+        }
+      std::sort(smp.begin(), smp.end());
+      c->pending_rows.push_back(h);
+      for (size_t r = 0; r < smp.size(); ++r) {
+        c->cnt[(size_t)(h - 1) * n + r] += 1;
+        c->tsum[(size_t)(h - 1) * n + r] += smp[r];
+      }
+      c->clock = s_next;
+      c->recorded++;
+      c->clocked++;
+    }
+    return DBW_OK;
+  }
   while (c->recorded < upto) {
     const int64_t u = c->recorded;
     int32_t h;
@@ -251,7 +286,10 @@ struct HostScope {
 // slot's previous reader, the choice kernel of iteration u-4, precedes the
 // choice of iteration u-2 that the fold waits for.
 dbw_status estimate(dbw_ctx* c, int64_t u) {
-  if (dbw_status s = fold(c, u, std::max<int64_t>(c->clocked, u - 1)); s != DBW_OK) return s;
+  // under Push & Wait the offsets of iteration u need the clock and the busy
+  // times after iteration u-1, so the fold goes through u-1 (waiting for k_{u-1})
+  const int64_t clock_upto = c->cfg.clock == DBW_CLOCK_PSW ? u : std::max<int64_t>(c->clocked, u - 1);
+  if (dbw_status s = fold(c, u, clock_upto); s != DBW_OK) return s;
   HostScope hs(c, DBW_KT_HOST_ESTIMATE);
   std::string why;
   double* hT = c->h_T + (size_t)(u % kSlots) * c->cfg.n;
@@ -502,6 +540,8 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   }
   c->cnt.assign((size_t)n * n, 0);
   c->tsum.assign((size_t)n * n, 0);
+  c->busy.assign(n, 0);
+  for (auto& v : c->offs) v.assign(n, 0);
   for (auto& v : c->sorted) v.assign(n, 0);
   c->T_scratch.assign(n, 0.0);
   reset_host_pipeline(c, 0, cf.n);
@@ -659,17 +699,31 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     if (dbw_status s = posted ? join_estimate(c) : estimate(c, t); s != DBW_OK) return s;
   }
   HostScope hq(c, DBW_KT_HOST_QUEUE);
-  // 2. this iteration's ticks and arrival order (workers by (tick, index))
-  //    into the pinned slot (its previous reader, the PS kernel of t-4,
-  //    precedes the one of t-2 the estimate waited for)
+  // 2. this iteration's arrival offsets and order (workers by (offset,
+  //    index)) into the pinned slot (its previous reader, the PS kernel of
+  //    t-4, precedes the one of t-2 the estimate waited for).  Under Push &
+  //    Wait the estimate just joined has folded iteration t-1, so the clock
+  //    and the busy times are those at the start of iteration t.
   int64_t* hk = c->h_ticks + (size_t)slot * n;
-  std::memcpy(hk, ticks_host, sizeof(int64_t) * n);
+  std::vector<int64_t>& off = c->offs[slot];
+  if (c->cfg.clock == DBW_CLOCK_PSW) {
+    if (c->recorded != t) return fail(c, DBW_ESTATE, "iteration %lld not folded before its offsets", (long long)t);
+    for (int i = 0; i < n; ++i) {
+      const int64_t wait = std::max<int64_t>(c->busy[i], c->clock) - c->clock;
+      if (ticks_host[i] >= (int64_t{1} << 48) - wait)
+        return fail(c, DBW_ERANGE, "arrival offset of worker %d reaches 2^48", i);
+      off[i] = wait + ticks_host[i];
+    }
+  } else {
+    std::memcpy(off.data(), ticks_host, sizeof(int64_t) * n);
+  }
+  std::memcpy(hk, off.data(), sizeof(int64_t) * n);
   int32_t* ho = c->h_order + (size_t)slot * n;
   for (int i = 0; i < n; ++i) ho[i] = i;
-  std::stable_sort(ho, ho + n, [&](int32_t a, int32_t b) { return ticks_host[a] < ticks_host[b]; });
+  std::stable_sort(ho, ho + n, [&](int32_t a, int32_t b) { return off[a] < off[b]; });
   std::vector<int64_t>& srt = c->sorted[slot];
   srt.resize(n);
-  for (int r = 0; r < n; ++r) srt[r] = ticks_host[ho[r]];
+  for (int r = 0; r < n; ++r) srt[r] = off[ho[r]];
   // 3. one PS kernel: the choice of k_t (T_hat read from the pinned slot, k_t
   //    written back into it), the first k_t arrivals, the aggregate and the
   //    update; then the statistics and the estimator bookkeeping (all on the
@@ -809,7 +863,30 @@ DBW_API dbw_status dbw_samples_import(dbw_ctx* c, const int64_t* cnt, const int6
   std::memcpy(c->cnt.data(), cnt, sizeof(int64_t) * c->cnt.size());
   std::memcpy(c->tsum.data(), tsum, sizeof(int64_t) * c->tsum.size());
   c->clock = clock;
+  std::fill(c->busy.begin(), c->busy.end(), clock);
   c->solver.reset();
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_busy_export(dbw_ctx* c, int64_t* busy) {
+  if (!c || !busy) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
+  DeviceGuard dg(c->device);
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
+  if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
+  std::memcpy(busy, c->busy.data(), sizeof(int64_t) * c->busy.size());
+  return DBW_OK;
+}
+
+DBW_API dbw_status dbw_busy_import(dbw_ctx* c, const int64_t* busy) {
+  if (!c || !busy) return DBW_EINVAL;
+  if (dbw_status s = join_estimate(c); s != DBW_OK) return s;
+  for (int i = 0; i < c->cfg.n; ++i)
+    if (busy[i] < 0) return fail(c, DBW_EINVAL, "busy time of worker %d is negative", i);
+  DeviceGuard dg(c->device);
+  if (dbw_status s = sync_all(c); s != DBW_OK) return s;
+  if (dbw_status s = fold(c, c->t, c->t); s != DBW_OK) return s;
+  std::memcpy(c->busy.data(), busy, sizeof(int64_t) * c->busy.size());
   return DBW_OK;
 }
 

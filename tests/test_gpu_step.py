@@ -104,6 +104,9 @@ def _lockstep(cfg, iters):
         st = orc.export_state()
         ctx.import_state(st)
         ctx.import_samples(np.array(st["cnt"], np.int64), np.array(st["tsum"], np.int64), st["clock"])
+        psw = cfg.clock == "psw"
+        if psw:
+            ctx.import_busy(np.array(orc.vclock.busy, np.int64))
         st_before = ctx.export_state()
         wd = to_dev(torch, w32)
         k_gpu = ctx.step(wd, Xd, yd, ticks, rows=to_dev(torch, idx), wait=True)
@@ -134,6 +137,8 @@ def _lockstep(cfg, iters):
             assert np.array_equal(cnt_g, np.array(orc.cnt, np.int64)), (cfg.name, t)
             assert np.array_equal(tsum_g, np.array(orc.tsum, np.int64)), (cfg.name, t)
             assert clock_g == orc.clock, (cfg.name, t)
+            if psw:
+                assert np.array_equal(ctx.export_busy(), np.array(orc.vclock.busy, np.int64)), (cfg.name, t)
     assert ties <= max(1, iters // 20), f"{ties} near-tie choices in {iters} iterations"
     return orc
 
@@ -155,6 +160,21 @@ def test_lockstep_mlp_32_workers_full_run():
     _lockstep(C4, C4.iters)
 
 
+def test_lockstep_push_and_wait_tiny():
+    # Push & Wait: late workers finish their stale gradient first, and
+    # workers still busy at a push skip it (censored samples)
+    orc = _lockstep(TINY.replace(clock="psw"), TINY.iters)
+    assert any(min(row) == 0 < max(row) for row in orc.cnt if max(row) > 0) or len(set(orc.ks)) > 1
+
+
+def test_lockstep_push_and_wait_16_workers_slow_pair():
+    # two workers five times slower: under Push & Wait they skip iterations
+    cfg = C2.replace(clock="psw")
+    orc = _lockstep(cfg, 60)
+    censored = sum(1 for row in orc.cnt for a, b in zip(row, row[1:]) if b < a)
+    assert censored > 0
+
+
 def test_lockstep_64_workers_first_iterations():
     _lockstep(C3, 12)
 
@@ -163,7 +183,7 @@ def test_lockstep_256_workers_100_classes_first_iterations():
     _lockstep(C5, 3)
 
 
-@pytest.mark.parametrize("cfg", [TINY, C1], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [TINY, C1, C2.replace(name="C2psw", clock="psw", iters=80)], ids=lambda c: c.name)
 def test_free_running_trajectory(cfg):
     X, y, ctx, Xd, yd = _setup(cfg)
     orc = odbw.DBWOracle(cfg, init_params(cfg))
