@@ -221,3 +221,42 @@ def test_estimator_falls_back_when_the_diagonal_binds(lib):
         np.testing.assert_array_equal(got, pb.time_estimate(cnt, tsum))
     st = est.stats()
     assert st["warm"] + st["full"] > 0, st
+
+
+def test_incremental_estimator_on_push_and_wait_rows(lib):
+    # Under Push & Wait a worker still busy at a push skips that iteration, so
+    # rows hold fewer than n samples and keep empty cells at their ends, and
+    # a row chosen once can sit below the diagonal chain.  The repairs must
+    # stay exact and converge without a full re-solve after the first one
+    # (an empty cell between two cells of a repair component must not cut
+    # the relation through it).
+    from oracle.clock import PsWClock
+    rng = np.random.default_rng(47)
+    n, iters = 24, 90
+    clk = PsWClock(n)
+    cnt = np.zeros((n, n), np.int64)
+    tsum = np.zeros((n, n), np.int64)
+    est = pb.TimeEstimator()
+    slow = rng.random(n) < 0.25
+    h = n
+    censored = 0
+    for t in range(iters):
+        tau = np.rint((1 + rng.exponential(1.0, size=n)) * np.where(slow, 4.0, 1.0) * 2 ** 16).astype(np.int64)
+        k = int(rng.choice([1, 2, 3, 5, 8, 12, 16, 20, 24], p=[.3, .15, .1, .1, .1, .08, .07, .05, .05]))
+        samples, _ = clk.advance(clk.offsets(tau), k)
+        censored += n - len(samples)
+        cnt[h - 1, :len(samples)] += 1
+        tsum[h - 1, :len(samples)] += samples
+        h = k
+        got = est.solve(cnt, tsum)
+        np.testing.assert_array_equal(got, pb.time_estimate(cnt, tsum))
+        if t % 6 == 5:
+            ref = te.time_estimate(cnt.tolist(), tsum.tolist())
+            for j in range(n):
+                if ref[j] is None:
+                    assert math.isnan(got[j])
+                else:
+                    assert got[j] == pytest.approx(ref[j], rel=1e-14, abs=0), (t, j)
+    assert censored > iters          # the rows really are censored
+    st = est.stats()
+    assert st["full"] <= 1, st
