@@ -130,8 +130,14 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C3")
-    ap.add_argument("--clock", choices=("fresh", "psw"), default="fresh",
-                    help="virtual clock: every worker starts each iteration afresh, or Push & Wait")
+    ap.add_argument("--clock", choices=("fresh", "psw", "psi"), default="fresh",
+                    help="virtual clock: every worker starts each iteration afresh, Push & Wait, "
+                         "or Push & Interrupt")
+    ap.add_argument("--policy", choices=("dbw", "static", "blind"), default="dbw",
+                    help="choice of k: DBW, a static k (--k-static), or B-DBW (gain = k)")
+    ap.add_argument("--k-static", type=int, default=0)
+    ap.add_argument("--estimator", choices=("isotonic", "naive"), default="isotonic",
+                    help="time estimate: constrained least squares, or the mean of cell (k,k)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true",
@@ -154,6 +160,10 @@ def main(argv=None) -> int:
     cfg = get(args.workload)
     if args.clock != cfg.clock:
         cfg = cfg.replace(clock=args.clock)
+    if args.policy == "static" and not 1 <= args.k_static <= cfg.n:
+        sys.exit(f"--policy static needs --k-static in [1, {cfg.n}]")
+    cfg = cfg.replace(policy=args.policy, k_static=args.k_static if args.policy == "static" else 0,
+                      estimator=args.estimator)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     if args.traffic_probe:
@@ -261,6 +271,7 @@ def main(argv=None) -> int:
             if cfg.model == "softmax" else
             f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows",
             "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P, "clock": cfg.clock,
+            "policy": cfg.policy, "k_static": cfg.k_static, "estimator": cfg.estimator,
         },
         "roofline": {
             "kernel": "worker gradients (dbw_worker_grads)",

@@ -71,7 +71,11 @@ class DBWConfig:
     seed: int = 14696           # base of the seed sequence
     labels: str = "uniform"     # "uniform" or "teacher" (test fixture)
     clock: str = "fresh"        # "fresh": every worker starts each iteration afresh;
-                                # "psw": Push & Wait, late workers finish their current gradient first
+                                # "psw": Push & Wait, late workers finish their current gradient first;
+                                # "psi": Push & Interrupt, late workers drop it (only k_t samples)
+    policy: str = "dbw"         # choice of k: "dbw", "static" (k_static), "blind" (B-DBW)
+    k_static: int = 0           # k of the static policy
+    estimator: str = "isotonic" # time estimate: "isotonic" or "naive" (mean of cell (k,k))
 
     @property
     def param_count(self) -> int:

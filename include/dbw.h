@@ -62,8 +62,26 @@ typedef enum { DBW_SOFTMAX = 0, DBW_MLP = 1 } dbw_model;
  * of iteration t and b_i the time worker i becomes free, worker i computes
  * w_t iff b_i <= s_t or b_i < s_{t+1}, its offset is
  * max(s_t, b_i) - s_t + tau_i, and a worker still busy at s_{t+1} skips w_t
- * (no sample: the estimate's data are censored). */
-typedef enum { DBW_CLOCK_FRESH = 0, DBW_CLOCK_PSW = 1 } dbw_clock;
+ * (no sample: the estimate's data are censored).  PSI (Push & Interrupt):
+ * the PS pushes w_{t+1} once it holds k_t gradients of w_t and every worker
+ * drops the gradient it is computing to start on w_{t+1}; offsets are the
+ * round-trip times as under FRESH, but only the first k_t arrivals in
+ * (offset, worker index) order complete, so only they are samples. */
+typedef enum { DBW_CLOCK_FRESH = 0, DBW_CLOCK_PSW = 1, DBW_CLOCK_PSI = 2 } dbw_clock;
+
+/* How k_t is chosen (Sect. 3.3; the settings compared in Sect. 4).
+ * DBW: Eqs. gain, greedy, greedy2.  STATIC: k_t = k_static at every
+ * iteration (a fixed number of backup workers); the objective is still
+ * computed as under DBW.  BLIND (B-DBW): the gain G_k is replaced by k and
+ * the rest of the rule is unchanged (k_t = n before the first smoothness
+ * estimate, the largest k among equal objectives, the loss guard). */
+typedef enum { DBW_POLICY_DBW = 0, DBW_POLICY_STATIC = 1, DBW_POLICY_BLIND = 2 } dbw_policy;
+
+/* Time estimate T_hat_k (Sect. 3.2).  ISOTONIC: from the solution of Eq.
+ * quadratic_opt (see dbw_time_estimate).  NAIVE: the empirical mean of the
+ * samples of cell (k,k), the first approach the section sets aside; NaN (k
+ * not eligible) while that cell holds no sample. */
+typedef enum { DBW_ESTIMATOR_ISOTONIC = 0, DBW_ESTIMATOR_NAIVE = 1 } dbw_estimator;
 
 #define DBW_MAX_N 1024 /* logical workers per context                       */
 #define DBW_MAX_D 64   /* length of the estimator averaging window D          */
@@ -71,14 +89,20 @@ typedef enum { DBW_CLOCK_FRESH = 0, DBW_CLOCK_PSW = 1 } dbw_clock;
 /* Problem description.  n workers, minibatch B per worker, d input features,
  * C classes, H hidden units (MLP only), learning rate eta (constant for all
  * k), window D of the estimator averages, loss guard factor beta >= 1
- * (Eq. greedy2), virtual clock (dbw_clock; 0 = fresh start).  S > 0 declares
+ * (Eq. greedy2), virtual clock (dbw_clock; 0 = fresh start), rule of the
+ * choice of k (dbw_policy; 0 = DBW) and time estimate (dbw_estimator; 0 =
+ * isotonic).  Zero-initialised fields give the method as defined.  S > 0 declares
  * a resident dataset of S rows that minibatches may index (see
  * dbw_worker_grads); S = 0 means minibatches are passed materialised. */
 typedef struct {
   int32_t model; /* dbw_model */
   int32_t n, B, d, C, H;
   int32_t D;
-  int32_t clock; /* dbw_clock */
+  int32_t clock;     /* dbw_clock */
+  int32_t policy;    /* dbw_policy */
+  int32_t k_static;  /* k of DBW_POLICY_STATIC, in [1, n]; ignored otherwise */
+  int32_t estimator; /* dbw_estimator */
+  int32_t reserved;  /* must be 0 */
   double eta, beta;
   int64_t S;
 } dbw_config;

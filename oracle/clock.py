@@ -27,6 +27,13 @@ over the workers that compute w_t.  A worker that becomes free exactly at
 s_{t+1} takes w_{t+1}.  The samples of iteration t are the sorted offsets of
 the workers that compute w_t (fewer than n when some skip: the censoring of
 the estimator's data).
+
+Push & Interrupt (the paper's PsI): the push of w_{t+1} interrupts every
+worker, which drops the gradient it is computing and starts on w_{t+1}.
+Every iteration therefore starts afresh, o_i = tau_{i,t}, but only the
+workers that deliver before the push complete: the first k_t in (offset,
+worker index) order.  Their offsets are the samples; the later n - k_t are
+censored.
 """
 from __future__ import annotations
 
@@ -69,9 +76,31 @@ class PsWClock:
         return samples, computed
 
 
+class PsIClock:
+    """Push & Interrupt: the push restarts every worker on the new vector."""
+
+    def __init__(self, n: int):
+        self.n = n
+        self.s = 0
+
+    def offsets(self, tau):
+        return [int(x) for x in tau]
+
+    def advance(self, offsets, k: int):
+        order = sorted(range(self.n), key=lambda i: (offsets[i], i))
+        done = order[:k]
+        self.s += offsets[order[k - 1]]
+        computed = [False] * self.n
+        for i in done:
+            computed[i] = True
+        return [offsets[i] for i in done], computed
+
+
 def make_clock(kind: str, n: int):
     if kind == "fresh":
         return FreshClock(n)
     if kind == "psw":
         return PsWClock(n)
+    if kind == "psi":
+        return PsIClock(n)
     raise ValueError(f"unknown clock {kind!r}")

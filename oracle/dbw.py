@@ -11,6 +11,12 @@ Choice of k_t at the start of iteration t (Sect. 3.3):
     k_{t-1} < n then k_t = max(k*, k_{t-1} + 1).
   * Before any L estimate exists (t = 0, 1) k_t = n; k_{-1} is taken as n.
 
+Variants the paper compares (Sect. 4): a static k (k_t = k_static at every
+iteration; the objective is still reported), and B-DBW, which takes the gain
+G_k = k (the number of aggregated gradients) and keeps the rest of the rule.
+The time estimate is the constrained one (Eq. quadratic_opt) or the naive
+mean of cell (k, k) (Sect. 3.2).
+
 End of iteration t (Sect. 3.1, Sect. 3.2):
   * push V+_t, N+_t, F_hat_t;
   * for t >= 1, L+_t = 2 (eta N+_{t-1} - (F_hat_{t-1} - F_hat_t))
@@ -30,7 +36,7 @@ import numpy as np
 
 from . import model, ps
 from .clock import make_clock
-from .time_estimator import time_estimate
+from .time_estimator import naive_estimate, time_estimate
 
 
 def window_mean(hist, D: int):
@@ -49,16 +55,22 @@ def gains(V: float, N: float, L: float, eta: float, n: int):
 
 
 def choose_k(n: int, eta: float, beta: float, D: int, hV, hN, hL, F_hist, k_prev: int,
-             T_hat):
+             T_hat, policy: str = "dbw", k_static: int = 0):
     """Returns (k_t, objective) with objective[k-1] = G_k / T_hat_k (None
-    before the first L estimate).  k whose T_hat_k is missing is not eligible."""
+    before the first L estimate).  k whose T_hat_k is missing is not eligible.
+    policy "blind" (B-DBW) uses G_k = k; "static" returns k_static."""
+    if policy not in ("dbw", "static", "blind"):
+        raise ValueError(f"unknown policy {policy!r}")
     if not hL:
         k_star, objective = n, None
     else:
-        V = window_mean(hV, D)
-        N = window_mean(hN, D)
-        L = window_mean(hL, D)
-        G = gains(V, N, L, eta, n)
+        if policy == "blind":
+            G = [float(k) for k in range(1, n + 1)]
+        else:
+            V = window_mean(hV, D)
+            N = window_mean(hN, D)
+            L = window_mean(hL, D)
+            G = gains(V, N, L, eta, n)
         objective = [(G[k - 1] / T_hat[k - 1]) if (T_hat[k - 1] is not None and T_hat[k - 1] > 0)
                      else None for k in range(1, n + 1)]
         eligible = [k for k in range(1, n + 1) if objective[k - 1] is not None]
@@ -70,6 +82,8 @@ def choose_k(n: int, eta: float, beta: float, D: int, hV, hN, hL, F_hist, k_prev
     k_t = k_star
     if len(F_hist) >= 2 and F_hist[-1] > beta * F_hist[-2] and k_prev < n:
         k_t = max(k_star, k_prev + 1)
+    if policy == "static":
+        k_t = k_static
     return k_t, objective
 
 
@@ -101,6 +115,8 @@ class DBWOracle:
 
     # -- pieces ------------------------------------------------------------
     def time_estimate(self):
+        if getattr(self.cfg, "estimator", "isotonic") == "naive":
+            return naive_estimate(self.cnt, self.tsum)
         if not any(any(r) for r in self.cnt):
             return [None] * self.cfg.n
         return time_estimate(self.cnt, self.tsum)
@@ -108,7 +124,8 @@ class DBWOracle:
     def choose(self, T_hat):
         c = self.cfg
         return choose_k(c.n, c.eta, c.beta, c.D, self.hV, self.hN, self.hL, self.F,
-                        self.k_prev, T_hat)
+                        self.k_prev, T_hat, policy=getattr(c, "policy", "dbw"),
+                        k_static=getattr(c, "k_static", 0))
 
     def record_times(self, offsets, k_t):
         """Bookkeeping of the arrival offsets of this iteration (row k_{t-1}):

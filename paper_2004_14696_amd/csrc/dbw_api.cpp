@@ -177,7 +177,15 @@ bool config_ok(const dbw_config* c, std::string* why) {
   else if (!(c->beta >= 1.0) || !std::isfinite(c->beta)) *why = "beta must be finite and >= 1";
   else if (c->S < 0 || c->S > (int64_t{1} << 31)) *why = "S outside [0, 2^31]";
   else if ((int64_t)c->n * c->B > (int64_t{1} << 30)) *why = "n*B too large";
-  else if (c->clock != DBW_CLOCK_FRESH && c->clock != DBW_CLOCK_PSW) *why = "clock must be DBW_CLOCK_FRESH or DBW_CLOCK_PSW";
+  else if (c->clock != DBW_CLOCK_FRESH && c->clock != DBW_CLOCK_PSW && c->clock != DBW_CLOCK_PSI)
+    *why = "clock must be DBW_CLOCK_FRESH, DBW_CLOCK_PSW or DBW_CLOCK_PSI";
+  else if (c->policy != DBW_POLICY_DBW && c->policy != DBW_POLICY_STATIC && c->policy != DBW_POLICY_BLIND)
+    *why = "policy must be DBW_POLICY_DBW, DBW_POLICY_STATIC or DBW_POLICY_BLIND";
+  else if (c->policy == DBW_POLICY_STATIC && (c->k_static < 1 || c->k_static > c->n))
+    *why = "k_static outside [1, n] under DBW_POLICY_STATIC";
+  else if (c->estimator != DBW_ESTIMATOR_ISOTONIC && c->estimator != DBW_ESTIMATOR_NAIVE)
+    *why = "estimator must be DBW_ESTIMATOR_ISOTONIC or DBW_ESTIMATOR_NAIVE";
+  else if (c->reserved != 0) *why = "reserved must be 0";
   else return true;
   return false;
 }
@@ -210,12 +218,13 @@ dbw_status known_k(dbw_ctx* c, int64_t u, int32_t* k) {
 }
 
 // Fold into the grid every iteration u < upto whose row k_{u-1} is known, and
-// into the clock every iteration u < clock_upto.  Under Push & Wait the
-// samples of iteration u depend on who computed w_u, which needs k_u and the
-// clock at u, so both advance together up to max(upto, clock_upto).
+// into the clock every iteration u < clock_upto.  Under Push & Wait and Push
+// & Interrupt the samples of iteration u depend on k_u (who computed w_u, who
+// completed before the push), so both advance together up to
+// max(upto, clock_upto).
 dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
   const int n = c->cfg.n;
-  if (c->cfg.clock == DBW_CLOCK_PSW) {
+  if (c->cfg.clock != DBW_CLOCK_FRESH) {
     const int64_t end = std::max(upto, clock_upto);
     while (c->recorded < end) {
       const int64_t u = c->recorded;
@@ -224,15 +233,20 @@ dbw_status fold(dbw_ctx* c, int64_t upto, int64_t clock_upto) {
       if (s == DBW_OK) s = known_k(c, u, &k);
       if (s != DBW_OK) return s;
       const std::vector<int64_t>& o = c->offs[u % kSlots];
-      const int64_t s_next = c->clock + c->sorted[u % kSlots][k - 1];
+      const std::vector<int64_t>& srt = c->sorted[u % kSlots];
+      const int64_t s_next = c->clock + srt[k - 1];
       std::vector<int64_t>& smp = c->psw_samples;
       smp.clear();
-      for (int i = 0; i < n; ++i)
-        if (c->busy[i] <= c->clock || c->busy[i] < s_next) {   // computed w_u
-          smp.push_back(o[i]);
-          c->busy[i] = c->clock + o[i];
-        }
-      std::sort(smp.begin(), smp.end());
+      if (c->cfg.clock == DBW_CLOCK_PSW) {
+        for (int i = 0; i < n; ++i)
+          if (c->busy[i] <= c->clock || c->busy[i] < s_next) {   // computed w_u
+            smp.push_back(o[i]);
+            c->busy[i] = c->clock + o[i];
+          }
+        std::sort(smp.begin(), smp.end());
+      } else {
+        smp.assign(srt.begin(), srt.begin() + k);   // the first k_u arrivals complete
+      }
       c->pending_rows.push_back(h);
       for (size_t r = 0; r < smp.size(); ++r) {
         c->cnt[(size_t)(h - 1) * n + r] += 1;
@@ -286,15 +300,25 @@ struct HostScope {
 // slot's previous reader, the choice kernel of iteration u-4, precedes the
 // choice of iteration u-2 that the fold waits for.
 dbw_status estimate(dbw_ctx* c, int64_t u) {
-  // under Push & Wait the offsets of iteration u need the clock and the busy
-  // times after iteration u-1, so the fold goes through u-1 (waiting for k_{u-1})
-  const int64_t clock_upto = c->cfg.clock == DBW_CLOCK_PSW ? u : std::max<int64_t>(c->clocked, u - 1);
+  // under Push & Wait and Push & Interrupt the samples of iteration u-1 need
+  // k_{u-1} (and under Push & Wait the offsets of iteration u the busy times
+  // after it), so the fold goes through u-1, waiting for k_{u-1}
+  const int64_t clock_upto = c->cfg.clock != DBW_CLOCK_FRESH ? u : std::max<int64_t>(c->clocked, u - 1);
   if (dbw_status s = fold(c, u, clock_upto); s != DBW_OK) return s;
   HostScope hs(c, DBW_KT_HOST_ESTIMATE);
   std::string why;
   double* hT = c->h_T + (size_t)(u % kSlots) * c->cfg.n;
-  if (c->solver.solve(c->cfg.n, c->cnt.data(), c->tsum.data(), hT, &why, &c->pending_rows) != 0)
+  if (c->cfg.estimator == DBW_ESTIMATOR_NAIVE) {
+    const int n = c->cfg.n;
+    // the mean of cell (k,k), correctly rounded (sums up to 2^52 convert exactly)
+    for (int k = 0; k < n; ++k) {
+      const int64_t m = c->cnt[(size_t)k * n + k], sum = c->tsum[(size_t)k * n + k];
+      if (sum > (int64_t{1} << 52)) return fail(c, DBW_ESTATE, "time estimate: a cell sum reaches beyond 2^52");
+      hT[k] = m > 0 ? static_cast<double>(sum) / static_cast<double>(m) : std::numeric_limits<double>::quiet_NaN();
+    }
+  } else if (c->solver.solve(c->cfg.n, c->cnt.data(), c->tsum.data(), hT, &why, &c->pending_rows) != 0) {
     return fail(c, DBW_ESTATE, "time estimate: %s", why.c_str());
+  }
   c->pending_rows.clear();
   return DBW_OK;
 }
@@ -665,6 +689,7 @@ DBW_API dbw_status dbw_choose_b(dbw_ctx* c, const double* T_hat, int32_t* k_out,
   ProfScope ps(c, DBW_KT_CHOOSE);
   dbw::ChooseArgs ca{};
   ca.st = c->st; ca.T_src = T_hat; ca.n = c->cfg.n; ca.eta = c->cfg.eta; ca.beta = c->cfg.beta;
+  ca.policy = c->cfg.policy; ca.k_static = c->cfg.k_static;
   ca.do_choose = 1; ca.do_select = 0; ca.k_out = k_out; ca.b_out = b_out; ca.objective = objective;
   ca.err = c->err;
   HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
@@ -735,7 +760,8 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
     ca.order_src = c->d_order + (size_t)slot * n;
     ca.T_hat = c->T_hat; ca.ticks = c->ticks; ca.k_host = c->d_k + slot; ca.n = n; ca.eta = c->cfg.eta;
-    ca.beta = c->cfg.beta; ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
+    ca.beta = c->cfg.beta; ca.policy = c->cfg.policy; ca.k_static = c->cfg.k_static;
+    ca.do_choose = 1; ca.do_select = 1; ca.k_out = c->k; ca.b_out = c->b;
     ca.objective = c->objective; ca.sel = c->sel; ca.mask = c->mask; ca.err = c->err;
     dbw::AggArgs aa{};
     aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;

@@ -100,6 +100,8 @@ struct ChooseArgs {
   int32_t* k_host;                // nullable pinned host copy of k
   int n;
   double eta, beta;
+  int policy;                     // dbw_policy
+  int k_static;                   // k under DBW_POLICY_STATIC
   int do_choose, do_select;
   int k_imm;                      // k when not choosing
   int32_t* k_out;                 // device (choose) -- also read by select

@@ -119,8 +119,9 @@ struct ChooseShared {
 };
 
 // The DBW choice of k_t from the staged state and T_hat (called by every
-// thread; wave 0 computes, k in sh.kfinal afterwards).  write: this block
-// stores k, b, the objective and the pinned copy of k.
+// thread; wave 0 computes, k in sh.kfinal afterwards).  B-DBW replaces the
+// gain by k; a static policy keeps the objective and overrides k.  write:
+// this block stores k, b, the objective and the pinned copy of k.
 __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
 #pragma clang fp contract(off)
   const int tid = threadIdx.x, lane = tid % WAVE;
@@ -142,8 +143,10 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
     double best_r = -INFINITY;
     int best_k = 0;
     double maxG = -INFINITY;
+    const bool blind = a.policy == DBW_POLICY_BLIND;
     for (int k = lane + 1; k <= n; k += WAVE) {
-      const double Gk = ga * N - gb * V / k;
+      // B-DBW takes the number of aggregated gradients as the gain
+      const double Gk = blind ? static_cast<double>(k) : ga * N - gb * V / k;
       const double T = sh.T[k - 1];
       const bool eligible = isfinite(T) && T > 0.0;
       const double r = eligible ? Gk / T : NAN;
@@ -171,6 +174,7 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
       int k = (!hasL || kb == 0 || g < 0.0) ? n : kb;
       // loss guard: never decrease k while the loss estimate rises
       if (st.nF >= 2 && st.F_prev > a.beta * st.F_prev2 && st.k_prev < n) k = max(k, st.k_prev + 1);
+      if (a.policy == DBW_POLICY_STATIC) k = a.k_static;
       if (write) {
         a.k_out[0] = k;
         a.b_out[0] = n - k;

@@ -92,9 +92,21 @@ def _compare_iteration(cfg, rec, out, k_gpu, w_prev32, w_new, st_before, st_afte
     return True
 
 
-def _lockstep(cfg, iters):
+def _seed_every_row(cfg, orc):
+    """One fresh-start sample set in every row h (as if each k had been used
+    once), from round-trip draws of iterations the run never reaches."""
+    for h in range(1, cfg.n + 1):
+        srt = sorted(int(x) for x in gen.round_trip_ticks(cfg, 10_000 + h))
+        for i, v in enumerate(srt):
+            orc.cnt[h - 1][i] += 1
+            orc.tsum[h - 1][i] += v
+
+
+def _lockstep(cfg, iters, seed_rows=False):
     X, y, ctx, Xd, yd = _setup(cfg)
     orc = odbw.DBWOracle(cfg, init_params(cfg))
+    if seed_rows:
+        _seed_every_row(cfg, orc)
     ties = 0
     for t in range(iters):
         idx = gen.batch_indices(cfg, t)
@@ -175,6 +187,38 @@ def test_lockstep_push_and_wait_16_workers_slow_pair():
     assert censored > 0
 
 
+def test_lockstep_static_k():
+    orc = _lockstep(TINY.replace(policy="static", k_static=3), 20)
+    assert orc.ks == [3] * 20
+
+
+def test_lockstep_blind_dbw():
+    # B-DBW: gain k, so k_t maximises k / T_hat_k
+    orc = _lockstep(TINY.replace(policy="blind"), TINY.iters)
+    assert orc.ks[:2] == [TINY.n] * 2 and len(set(orc.ks)) > 1
+
+
+def test_lockstep_blind_dbw_push_interrupt_16_workers():
+    orc = _lockstep(C2.replace(policy="blind", clock="psi"), 60)
+    assert sum(map(sum, orc.cnt)) == sum(orc.ks)    # exactly k_t samples per iteration
+
+
+def test_lockstep_naive_estimator():
+    # the diagonal means of a grid seeded with one sample set per row, then
+    # the run's own samples
+    orc = _lockstep(TINY.replace(estimator="naive"), TINY.iters, seed_rows=True)
+    assert len(set(orc.ks)) > 1
+
+
+def test_lockstep_naive_estimator_push_and_wait_16_workers():
+    _lockstep(C2.replace(estimator="naive", clock="psw"), 60, seed_rows=True)
+
+
+def test_lockstep_push_interrupt_tiny():
+    orc = _lockstep(TINY.replace(clock="psi"), TINY.iters)
+    assert len(set(orc.ks)) > 1
+
+
 def test_lockstep_64_workers_first_iterations():
     _lockstep(C3, 12)
 
@@ -183,7 +227,9 @@ def test_lockstep_256_workers_100_classes_first_iterations():
     _lockstep(C5, 3)
 
 
-@pytest.mark.parametrize("cfg", [TINY, C1, C2.replace(name="C2psw", clock="psw", iters=80)], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [TINY, C1, C2.replace(name="C2psw", clock="psw", iters=80),
+                                 C2.replace(name="C2psi_blind", clock="psi", policy="blind", iters=80)],
+                         ids=lambda c: c.name)
 def test_free_running_trajectory(cfg):
     X, y, ctx, Xd, yd = _setup(cfg)
     orc = odbw.DBWOracle(cfg, init_params(cfg))

@@ -7,7 +7,7 @@ import heapq
 import numpy as np
 import pytest
 
-from oracle.clock import FreshClock, PsWClock, make_clock
+from oracle.clock import FreshClock, PsIClock, PsWClock, make_clock
 
 
 def test_psw_hand_worked_case():
@@ -132,3 +132,38 @@ def test_psw_censoring_invariants():
                 assert c.busy[i] == s0 + o[i]
     with pytest.raises(ValueError):
         make_clock("sundial", 2)
+
+
+def test_psi_hand_worked_case():
+    # n = 3, tau = (2, 5, 9), k = 2: workers 0 and 1 deliver at 2 and 5, the
+    # push at 5 interrupts worker 2.  Then tau = (4, 4, 4), k = 2: ties by
+    # index, worker 2 is interrupted at the push at 5 + 4 = 9.
+    c = make_clock("psi", 3)
+    o = c.offsets([2, 5, 9])
+    assert o == [2, 5, 9]
+    assert c.advance(o, 2) == ([2, 5], [True, True, False]) and c.s == 5
+    o = c.offsets([4, 4, 4])
+    assert c.advance(o, 2) == ([4, 4], [True, True, False]) and c.s == 9
+    o = c.offsets([7, 1, 3])
+    assert c.advance(o, 1) == ([1], [False, True, False]) and c.s == 10
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_psi_is_fresh_start_censored_at_k(seed):
+    # Every push restarts all workers, so the timing is the fresh-start one;
+    # only the first k_t arrivals (by offset, then index, as the PS selects)
+    # complete.
+    from oracle.ps import select_fastest
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(2, 12))
+    a, b = PsIClock(n), FreshClock(n)
+    for _ in range(40):
+        tau = rng.integers(1, 30, size=n)           # small range: many ties
+        k = int(rng.integers(1, n + 1))
+        oa, ob = a.offsets(tau), b.offsets(tau)
+        assert oa == ob
+        samples, computed = a.advance(oa, k)
+        fresh, _ = b.advance(ob, k)
+        assert samples == fresh[:k] and a.s == b.s
+        _, mask = select_fastest(oa, k)
+        assert computed == [bool(m) for m in mask]

@@ -153,3 +153,64 @@ def test_static_full_sync_is_plain_sgd():
         Gu, _ = model.softmax_worker_grads(w, Xt.reshape(1, -1, cfg.d), yt.reshape(1, -1), cfg.C)
         w = w - cfg.eta * Gu[0]
         np.testing.assert_allclose(orc.w, w, rtol=1e-12, atol=1e-15)
+
+
+def _choose_policy(n, V, N, L, T_hat, policy, k_static=0, F=(1.0, 1.0), k_prev=None, hL=True):
+    k_prev = n if k_prev is None else k_prev
+    return dbw.choose_k(n, 0.1, 1.01, 5, [V], [N], [L] if hL else [], list(F), k_prev, T_hat,
+                        policy=policy, k_static=k_static)
+
+
+def test_blind_gain_is_k_per_unit_time():
+    # B-DBW: objective k / T_hat_k = (1, 4/3, 1.2, 1) -> k = 2, whatever the
+    # gradient statistics say (here they make DBW pick k = 1).
+    T = [1.0, 1.5, 2.5, 4.0]
+    k, obj = _choose_policy(4, 3.0, 0.1, -5.0, T, "blind")
+    assert k == 2
+    assert obj == [1.0 / 1.0, 2.0 / 1.5, 3.0 / 2.5, 4.0 / 4.0]
+    assert _choose(4, 3.0, 0.1, -5.0, T)[0] == 1
+    # all DBW gains negative (N = 0): DBW waits for all, B-DBW still maximises k / T
+    assert _choose(4, 4.0, 0.0, 2.0, T)[0] == 4
+    assert _choose_policy(4, 4.0, 0.0, 2.0, T, "blind")[0] == 2
+
+
+def test_blind_ties_go_to_largest_k_and_rest_of_rule_holds():
+    k, _ = _choose_policy(5, 1.0, 1.0, 1.0, [1.0, 2.0, 3.0, 4.0, 5.0], "blind")   # k / k = 1 for all k
+    assert k == 5
+    # before the first smoothness estimate: n
+    k, obj = _choose_policy(5, 1.0, 1.0, 1.0, [1.0, 2.0, 3.0, 4.0, 5.0], "blind", hL=False)
+    assert k == 5 and obj is None
+    # the loss guard still applies
+    T = [1.0, 1.5, 2.5, 4.0, 8.0]
+    assert _choose_policy(5, 1.0, 1.0, 1.0, T, "blind", k_prev=3)[0] == 2
+    assert _choose_policy(5, 1.0, 1.0, 1.0, T, "blind", F=(1.0, 1.02), k_prev=3)[0] == 4
+    # missing estimates are not eligible
+    assert _choose_policy(4, 1.0, 1.0, 1.0, [None, 1.5, None, 4.0], "blind")[0] == 2
+
+
+def test_static_policy_overrides_the_choice_and_keeps_the_objective():
+    T = [1.0, 1.5, 2.0, 2.5, 3.0, 3.5]
+    k_dbw, obj_dbw = _choose(6, 3.0, 0.1, -5.0, T, F=(1.0, 1.02), k_prev=3)
+    for ks in (1, 3, 6):
+        k, obj = _choose_policy(6, 3.0, 0.1, -5.0, T, "static", k_static=ks, F=(1.0, 1.02), k_prev=3)
+        assert k == ks and obj == obj_dbw
+    k, obj = _choose_policy(6, 3.0, 0.1, -5.0, T, "static", k_static=2, hL=False)
+    assert k == 2 and obj is None
+    with pytest.raises(ValueError):
+        _choose_policy(6, 3.0, 0.1, -5.0, T, "oracle")
+
+
+def test_static_policy_trajectory_and_push_interrupt_rows():
+    # A static run keeps k; under Push & Interrupt each iteration leaves
+    # exactly k_t samples in row k_{t-1} (k_{-1} = n).
+    cfg = _tiny_cfg(policy="static", k_static=2, clock="psi")
+    X, y = gen.dataset(cfg)
+    orc = dbw.DBWOracle(cfg, init_params(cfg))
+    for t in range(5):
+        Xt, yt = gather(X, y, gen.batch_indices(cfg, t))
+        rec = orc.step(Xt, yt, gen.round_trip_ticks(cfg, t))
+        assert rec["k"] == 2 and sum(rec["computed"]) == 2
+    cnt = np.array(orc.cnt)
+    assert cnt[cfg.n - 1].tolist() == [1, 1] + [0] * (cfg.n - 2)      # iteration 0, row n
+    assert cnt[1].tolist() == [4, 4] + [0] * (cfg.n - 2)              # iterations 1-4, row 2
+    assert cnt.sum() == 2 * 5

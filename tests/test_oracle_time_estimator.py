@@ -262,3 +262,31 @@ def test_solution_is_feasible_and_blockwise_mean():
             tot_c = sum(cnt[h - 1][k - 1] for h, k in cells)
             tot_s = sum(tsum[h - 1][k - 1] for h, k in cells)
             assert Fraction(tot_s, tot_c) == x
+
+
+def test_naive_estimate_hand_worked_case():
+    # n = 3.  Row 1: counts (2, 2, 2), sums (2, 6, 10) -> means (1, 3, 5).
+    # Row 3: counts (1, 1, 1), sums (4, 5, 6).  The naive estimate reads the
+    # diagonal: T_1 = cell (1,1) = 1, T_2 = cell (2,2) (empty) -> None,
+    # T_3 = cell (3,3) = 6.  The constrained estimate pools the violated
+    # diagonal relation x_{1,1} <= ... and has a value for every k.
+    cnt = [[2, 2, 2], [0, 0, 0], [1, 1, 1]]
+    tsum = [[2, 6, 10], [0, 0, 0], [4, 5, 6]]
+    assert te.naive_estimate(cnt, tsum) == [1.0, None, 6.0]
+    iso = te.time_estimate(cnt, tsum)
+    assert None not in iso
+    # quotients are rounded once: 1/3 of a tick is the double nearest 1/3
+    assert te.naive_estimate([[3]], [[1]]) == [1 / 3]
+    assert te.naive_estimate([[3]], [[2 ** 52 + 1]]) == [float(Fraction(2 ** 52 + 1, 3))]
+
+
+def test_naive_estimate_equals_constrained_one_on_consistent_full_grids():
+    # With every row sampled and means x_{h,k} = 10 k - h (every constraint
+    # slack) the fit is the empirical mean, and T_hat_k is the fit at (k,k).
+    rng = np.random.default_rng(33)
+    for _ in range(10):
+        n = int(rng.integers(2, 8))
+        cnt = [[int(rng.integers(1, 4)) for _ in range(n)] for _ in range(n)]
+        tsum = [[cnt[h][k] * (10 * (k + 1) - (h + 1)) for k in range(n)] for h in range(n)]
+        assert te.naive_estimate(cnt, tsum) == te.time_estimate(cnt, tsum) == \
+            [float(10 * k - k) for k in range(1, n + 1)]
