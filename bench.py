@@ -138,6 +138,10 @@ def main(argv=None) -> int:
     ap.add_argument("--k-static", type=int, default=0)
     ap.add_argument("--estimator", choices=("isotonic", "naive"), default="isotonic",
                     help="time estimate: constrained least squares, or the mean of cell (k,k)")
+    ap.add_argument("--g-rows", choices=("all", "selected", "none"), default="all",
+                    help="worker-gradient rows a step writes; with selected/none the selected "
+                         "workers' slab partials are aggregated in one kernel where the softmax "
+                         "kernel splits rows into slabs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-kernel-timing", action="store_true",
@@ -163,7 +167,7 @@ def main(argv=None) -> int:
     if args.policy == "static" and not 1 <= args.k_static <= cfg.n:
         sys.exit(f"--policy static needs --k-static in [1, {cfg.n}]")
     cfg = cfg.replace(policy=args.policy, k_static=args.k_static if args.policy == "static" else 0,
-                      estimator=args.estimator)
+                      estimator=args.estimator, g_rows=args.g_rows)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     if args.traffic_probe:
@@ -271,7 +275,7 @@ def main(argv=None) -> int:
             if cfg.model == "softmax" else
             f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows",
             "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P, "clock": cfg.clock,
-            "policy": cfg.policy, "k_static": cfg.k_static, "estimator": cfg.estimator,
+            "policy": cfg.policy, "k_static": cfg.k_static, "estimator": cfg.estimator, "g_rows": cfg.g_rows,
         },
         "roofline": {
             "kernel": "worker gradients (dbw_worker_grads)",

@@ -76,6 +76,7 @@ class DBWConfig:
     policy: str = "dbw"         # choice of k: "dbw", "static" (k_static), "blind" (B-DBW)
     k_static: int = 0           # k of the static policy
     estimator: str = "isotonic" # time estimate: "isotonic" or "naive" (mean of cell (k,k))
+    g_rows: str = "all"         # worker-gradient rows a GPU step writes: "all", "selected", "none"
 
     @property
     def param_count(self) -> int:

@@ -83,6 +83,19 @@ typedef enum { DBW_POLICY_DBW = 0, DBW_POLICY_STATIC = 1, DBW_POLICY_BLIND = 2 }
  * not eligible) while that cell holds no sample. */
 typedef enum { DBW_ESTIMATOR_ISOTONIC = 0, DBW_ESTIMATOR_NAIVE = 1 } dbw_estimator;
 
+/* Rows of the worker-gradient buffer that dbw_step writes (the PS only uses
+ * the k_t fastest gradients, Eq. grad_bw).  ALL: every worker's row (the
+ * aggregation then reads the selected ones back).  SELECTED: only the
+ * selected workers' rows; NONE: no row.  With SELECTED or NONE, wherever the
+ * softmax gradient kernel splits a worker's minibatch into several row slabs,
+ * one kernel sums the selected workers' slab partials and aggregates them
+ * directly, so the unselected rows are never formed and no row is read back;
+ * g_t, the updated w, the losses, k and the mask are bitwise those of ALL,
+ * the statistics equal up to the order of their fp64 and fp32 partial sums.
+ * Rows not written hold unspecified values after dbw_step.  dbw_worker_grads
+ * always writes every row. */
+typedef enum { DBW_G_ROWS_ALL = 0, DBW_G_ROWS_SELECTED = 1, DBW_G_ROWS_NONE = 2 } dbw_g_rows;
+
 #define DBW_MAX_N 1024 /* logical workers per context                       */
 #define DBW_MAX_D 64   /* length of the estimator averaging window D          */
 
@@ -91,7 +104,8 @@ typedef enum { DBW_ESTIMATOR_ISOTONIC = 0, DBW_ESTIMATOR_NAIVE = 1 } dbw_estimat
  * k), window D of the estimator averages, loss guard factor beta >= 1
  * (Eq. greedy2), virtual clock (dbw_clock; 0 = fresh start), rule of the
  * choice of k (dbw_policy; 0 = DBW) and time estimate (dbw_estimator; 0 =
- * isotonic).  Zero-initialised fields give the method as defined.  S > 0 declares
+ * isotonic), rows of G that dbw_step writes (dbw_g_rows; 0 = all).
+ * Zero-initialised fields give the method as defined.  S > 0 declares
  * a resident dataset of S rows that minibatches may index (see
  * dbw_worker_grads); S = 0 means minibatches are passed materialised. */
 typedef struct {
@@ -102,7 +116,7 @@ typedef struct {
   int32_t policy;    /* dbw_policy */
   int32_t k_static;  /* k of DBW_POLICY_STATIC, in [1, n]; ignored otherwise */
   int32_t estimator; /* dbw_estimator */
-  int32_t reserved;  /* must be 0 */
+  int32_t g_rows;    /* dbw_g_rows */
   double eta, beta;
   int64_t S;
 } dbw_config;

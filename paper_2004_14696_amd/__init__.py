@@ -17,4 +17,5 @@ def config_from(wl, S: int = 0) -> Config:
     """C-ABI configuration for a workload description (dbw_inputs.DBWConfig)."""
     return make_config(wl.model, wl.n, wl.B, wl.d, wl.C, wl.H, eta=wl.eta, beta=wl.beta, D=wl.D, S=S,
                        clock=getattr(wl, "clock", "fresh"), policy=getattr(wl, "policy", "dbw"),
-                       k_static=getattr(wl, "k_static", 0), estimator=getattr(wl, "estimator", "isotonic"))
+                       k_static=getattr(wl, "k_static", 0), estimator=getattr(wl, "estimator", "isotonic"),
+                       g_rows=getattr(wl, "g_rows", "all"))

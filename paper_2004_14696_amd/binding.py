@@ -22,6 +22,7 @@ DBW_SOFTMAX, DBW_MLP = 0, 1
 DBW_CLOCK_FRESH, DBW_CLOCK_PSW, DBW_CLOCK_PSI = 0, 1, 2
 DBW_POLICY_DBW, DBW_POLICY_STATIC, DBW_POLICY_BLIND = 0, 1, 2
 DBW_ESTIMATOR_ISOTONIC, DBW_ESTIMATOR_NAIVE = 0, 1
+DBW_G_ROWS_ALL, DBW_G_ROWS_SELECTED, DBW_G_ROWS_NONE = 0, 1, 2
 DBW_MAX_N, DBW_MAX_D = 1024, 64
 DBW_KT_GRADS, DBW_KT_AGGREGATE, DBW_KT_CHOOSE, DBW_KT_HOST_ESTIMATE, DBW_KT_HOST_STEP = 0, 1, 2, 3, 4
 DBW_KT_HOST_WAIT, DBW_KT_HOST_QUEUE = 5, 6
@@ -49,7 +50,7 @@ class Config(ctypes.Structure):
     _fields_ = [("model", c_int32), ("n", c_int32), ("B", c_int32), ("d", c_int32),
                 ("C", c_int32), ("H", c_int32), ("D", c_int32), ("clock", c_int32),
                 ("policy", c_int32), ("k_static", c_int32), ("estimator", c_int32),
-                ("reserved", c_int32), ("eta", c_double), ("beta", c_double), ("S", c_int64)]
+                ("g_rows", c_int32), ("eta", c_double), ("beta", c_double), ("S", c_int64)]
 
 
 class IterStats(ctypes.Structure):
@@ -138,12 +139,13 @@ def load_library(path: str = LIB_PATH):
 CLOCKS = {"fresh": DBW_CLOCK_FRESH, "psw": DBW_CLOCK_PSW, "psi": DBW_CLOCK_PSI}
 POLICIES = {"dbw": DBW_POLICY_DBW, "static": DBW_POLICY_STATIC, "blind": DBW_POLICY_BLIND}
 ESTIMATORS = {"isotonic": DBW_ESTIMATOR_ISOTONIC, "naive": DBW_ESTIMATOR_NAIVE}
+G_ROWS = {"all": DBW_G_ROWS_ALL, "selected": DBW_G_ROWS_SELECTED, "none": DBW_G_ROWS_NONE}
 
 
 def make_config(model: str | int, n: int, B: int, d: int, C: int, H: int = 0, eta: float = 0.1,
                 beta: float = 1.01, D: int = 5, S: int = 0, clock: str | int = DBW_CLOCK_FRESH,
                 policy: str | int = DBW_POLICY_DBW, k_static: int = 0,
-                estimator: str | int = DBW_ESTIMATOR_ISOTONIC) -> Config:
+                estimator: str | int = DBW_ESTIMATOR_ISOTONIC, g_rows: str | int = DBW_G_ROWS_ALL) -> Config:
     if isinstance(model, str):
         model = {"softmax": DBW_SOFTMAX, "mlp": DBW_MLP}[model]
     if isinstance(clock, str):
@@ -152,8 +154,10 @@ def make_config(model: str | int, n: int, B: int, d: int, C: int, H: int = 0, et
         policy = POLICIES[policy]
     if isinstance(estimator, str):
         estimator = ESTIMATORS[estimator]
+    if isinstance(g_rows, str):
+        g_rows = G_ROWS[g_rows]
     return Config(model=model, n=n, B=B, d=d, C=C, H=H, D=D, clock=clock, policy=policy,
-                  k_static=k_static, estimator=estimator, reserved=0, eta=eta, beta=beta, S=S)
+                  k_static=k_static, estimator=estimator, g_rows=g_rows, eta=eta, beta=beta, S=S)
 
 
 def param_count(cfg: Config) -> int:

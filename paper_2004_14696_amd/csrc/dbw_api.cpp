@@ -55,6 +55,10 @@ struct dbw_ctx {
   dbw::SoftmaxPlan splan;
   dbw::MlpPlan mplan;
   int64_t agg_nblocks = 0;
+  // dbw_step aggregates the slab partials directly (g_rows not ALL, softmax
+  // single pass with several slabs per worker): source and column tiles
+  int slab_src = 0;
+  int64_t slab_nblocks = 0;
 
   char* pool = nullptr;
   // device buffers (carved from pool)
@@ -185,7 +189,8 @@ bool config_ok(const dbw_config* c, std::string* why) {
     *why = "k_static outside [1, n] under DBW_POLICY_STATIC";
   else if (c->estimator != DBW_ESTIMATOR_ISOTONIC && c->estimator != DBW_ESTIMATOR_NAIVE)
     *why = "estimator must be DBW_ESTIMATOR_ISOTONIC or DBW_ESTIMATOR_NAIVE";
-  else if (c->reserved != 0) *why = "reserved must be 0";
+  else if (c->g_rows != DBW_G_ROWS_ALL && c->g_rows != DBW_G_ROWS_SELECTED && c->g_rows != DBW_G_ROWS_NONE)
+    *why = "g_rows must be DBW_G_ROWS_ALL, DBW_G_ROWS_SELECTED or DBW_G_ROWS_NONE";
   else return true;
   return false;
 }
@@ -407,7 +412,7 @@ dbw_status sync_all(dbw_ctx* c) {
 }
 
 dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_t* y, const int32_t* rows,
-                        float* G, float* loss) {
+                        float* G, float* loss, bool keep_slabs = false) {
   ProfScope ps(c, DBW_KT_GRADS);
   const dbw_config& cf = c->cfg;
   hipError_t e;
@@ -418,6 +423,7 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.G = G; a.loss = loss;
     a.Gp = c->Gp; a.lossp = c->lossp; a.Z = c->Z; a.ce = c->ce;
     a.err = c->err;
+    a.keep_slabs = keep_slabs ? 1 : 0;
     e = dbw::launch_softmax_grads(c->splan, a, c->stream);
   } else {
     dbw::MlpArgs a{};
@@ -487,6 +493,12 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
     }
   }
   c->agg_nblocks = dbw::agg_blocks(P);
+  if (cf.g_rows != DBW_G_ROWS_ALL && cf.model == DBW_SOFTMAX && c->splan.fused && c->splan.slabs > 1 &&
+      c->splan.part % 4 == 0 && dbw::agg_blocks(c->splan.part) <= dbw::kStepPsMaxBlocks) {
+    c->slab_src = c->splan.fused == 2 ? dbw::SRC_SLAB_TILES : dbw::SRC_SLABS;
+    c->slab_nblocks = dbw::agg_blocks(c->splan.part);
+  }
+  const int64_t part_blocks = std::max(c->agg_nblocks, c->slab_nblocks);
 
   // workspace layout
   std::vector<Span> spans;
@@ -503,7 +515,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
        sT = take(sizeof(double) * n), sObj = take(sizeof(double) * n), sK = take(4), sB = take(4),
        sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
        sSt = take(sizeof(dbw_estimator_state)), sErr = take(4),
-       sSqp = take(sizeof(float) * n * c->agg_nblocks), sPart = take(sizeof(double) * 2 * c->agg_nblocks);
+       sSqp = take(sizeof(float) * n * part_blocks), sPart = take(sizeof(double) * 2 * part_blocks);
   Span sGp, sLp, sZ, sCe, sH, sdA;
   if (cf.model == DBW_SOFTMAX) {
     if (c->splan.fused) {
@@ -715,7 +727,9 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   //    waits for T_hat_t.  loss alternates halves by step parity (the
   //    statistics of step t-1 may still read the other half).
   float* loss = c->loss + (size_t)(t & 1) * n;
-  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss); s != DBW_OK) return s;
+  //    With a slab source the partials stay for the PS kernel.
+  const bool slab = c->slab_src != 0;
+  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss, slab); s != DBW_OK) return s;
   // 1. T_hat_t in the pinned slot: solved by the worker since k_{t-2} became
   //    known, or here when no job was posted (first step of a history)
   {
@@ -766,9 +780,15 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     dbw::AggArgs aa{};
     aa.G = c->G; aa.P = c->P; aa.n = n; aa.sel = c->sel; aa.k_dev = c->k; aa.g_out = c->g; aa.w = w;
     aa.eta = static_cast<float>(c->cfg.eta); aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_FUSED;
+    if (slab) {
+      aa.src = c->slab_src; aa.Gp = c->Gp; aa.slabs = c->splan.slabs; aa.slab_len = c->splan.part;
+      aa.d = c->cfg.d; aa.C = c->cfg.C; aa.B = c->cfg.B; aa.lossp = c->lossp; aa.loss = loss;
+      aa.G_rows = c->cfg.g_rows == DBW_G_ROWS_SELECTED ? c->G : nullptr;
+    }
     // every block of the fused kernel repeats the choice; beyond about two
-    // blocks per CU the separate choice kernel is cheaper
-    const bool fused = c->agg_nblocks <= dbw::kStepPsMaxBlocks;
+    // blocks per CU the separate choice kernel is cheaper (the slab source
+    // is only taken within that bound)
+    const bool fused = slab || c->agg_nblocks <= dbw::kStepPsMaxBlocks;
     if (fused) {
       HIP_TRY(c, dbw::launch_step_ps(ca, aa, c->stream));
     } else {
@@ -781,7 +801,8 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     c->t = t + 1;
     post_estimate(c, t + 1);
     dbw::FinalizeArgs fa{};
-    fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = c->agg_nblocks; fa.mask = c->mask; fa.k_dev = c->k;
+    fa.sqpart = c->sqpart; fa.part = c->part; fa.nblocks = slab ? c->slab_nblocks : c->agg_nblocks;
+    fa.mask = c->mask; fa.k_dev = c->k;
     fa.loss = loss; fa.n = n; fa.sqnorm = c->sqnorm; fa.stats = c->stats; fa.st = c->st;
     fa.eta = c->cfg.eta; fa.D = c->cfg.D; fa.bookkeeping = 1; fa.err = c->err;
     HIP_TRY(c, dbw::launch_finalize(fa, c->stream));

@@ -64,6 +64,7 @@ struct SoftmaxArgs {
   float* Z;              // [n*B][C] logits / residuals (GEMM path)
   float* ce;             // [n*B] per-row CE (GEMM path)
   int32_t* err;
+  int keep_slabs;        // 1: leave the slab partials for the PS kernel (no slab reduction)
 };
 
 SoftmaxPlan softmax_plan(int n, int B, int d, int C);
@@ -128,7 +129,20 @@ struct AggArgs {
   float* sqpart;        // [n][nblocks]
   double* part;         // [nblocks][2]
   int mode;
+  // k_step_ps only: where worker j's gradient row comes from
+  int src;              // AggSrc
+  const float* Gp;      // SRC_SLABS*: slab partials, worker j's slab q at (j slabs + q) slab_len
+  int slabs;
+  int64_t slab_len;     // floats of one slab partial (a multiple of 4)
+  int d, C, B;
+  const float* lossp;   // [n][slabs] slab loss sums -> loss[n] (the mean over B)
+  float* loss;
+  float* G_rows;        // nullable: the selected rows are written here in [d][C] order
 };
+// Gradient rows of k_step_ps: the G rows themselves, or the sum of a worker's
+// slab partials in slab order, laid out as [d][C] or in the matrix-core
+// kernel's tile order (64-feature groups; see k_softmax.hip).
+enum AggSrc { SRC_ROWS = 0, SRC_SLABS = 1, SRC_SLAB_TILES = 2 };
 hipError_t launch_aggregate(const AggArgs& a, hipStream_t s);
 // Choice, selection by the host-sorted arrival order, and fused aggregation
 // in one launch (dbw_step); ca.order_src must be set.  Used up to this many

@@ -67,6 +67,16 @@ __device__ __forceinline__ double readlane_d(double v, int l) {
   return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
 }
 
+// Sum over each row of 16 lanes by a DPP butterfly, in every lane of the row
+// (a fixed order, so the result is reproducible).
+__device__ __forceinline__ double row_sum_d(double v) {
+  v += dpp_d<0xB1>(v);
+  v += dpp_d<0x4E>(v);
+  v += dpp_d<0x141>(v);
+  v += dpp_d<0x140>(v);
+  return v;
+}
+
 // Fixed-order sums of doubles over the block (blockDim.x a multiple of 64,
 // at most 1024), M at a time; the results in all threads.
 template <int M>
@@ -103,14 +113,6 @@ __device__ __forceinline__ void store_state(const dbw_estimator_state* sh, dbw_e
   for (int i = threadIdx.x; i < W; i += blockDim.x) dst[i] = src[i];
 }
 
-// (objective, k) of the better choice: larger objective, then larger k.
-__device__ __forceinline__ void better(double& r, int& k, double r2, int k2) {
-  if (k2 != 0 && (k == 0 || r2 > r || (r2 == r && k2 > k))) {
-    r = r2;
-    k = k2;
-  }
-}
-
 // LDS of the choice of k.
 struct ChooseShared {
   dbw_estimator_state st;
@@ -140,9 +142,11 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
     const bool hasL = st.nL > 0;
     const double ga = a.eta - L * a.eta * a.eta / 2.0;
     const double gb = L * a.eta * a.eta / 2.0;
+    // each lane's best (objective, k) over k = lane + 1 + 64 m: ties go to
+    // the later, larger k
     double best_r = -INFINITY;
     int best_k = 0;
-    double maxG = -INFINITY;
+    bool nonneg = false;   // some gain >= 0
     const bool blind = a.policy == DBW_POLICY_BLIND;
     for (int k = lane + 1; k <= n; k += WAVE) {
       // B-DBW takes the number of aggregated gradients as the gain
@@ -151,27 +155,33 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
       const bool eligible = isfinite(T) && T > 0.0;
       const double r = eligible ? Gk / T : NAN;
       if (write && a.objective) a.objective[k - 1] = hasL ? r : NAN;
-      maxG = fmax(maxG, Gk);
-      if (eligible) better(best_r, best_k, r, k);
+      nonneg = nonneg || Gk >= 0.0;
+      const bool take = eligible && !isnan(r) && (best_k == 0 || r >= best_r);
+      best_r = take ? r : best_r;
+      best_k = take ? k : best_k;
     }
-    // the best (objective, k) and the largest gain: within rows of 16 lanes,
-    // then over the four rows (both selections are exact)
-#define DBW_CHOOSE_STEP(CTRL)                                   \
-    better(best_r, best_k, dpp_d<CTRL>(best_r), dpp_i<CTRL>(best_k)); \
-    maxG = fmax(maxG, dpp_d<CTRL>(maxG));
-    DBW_CHOOSE_STEP(0xB1)
-    DBW_CHOOSE_STEP(0x4E)
-    DBW_CHOOSE_STEP(0x141)
-    DBW_CHOOSE_STEP(0x140)
-#undef DBW_CHOOSE_STEP
-    double r = readlane_d(best_r, 0), g = readlane_d(maxG, 0);
-    int kb = __builtin_amdgcn_readlane(best_k, 0);
-    for (int row = 1; row < 4; ++row) {
-      better(r, kb, readlane_d(best_r, 16 * row), __builtin_amdgcn_readlane(best_k, 16 * row));
-      g = fmax(g, readlane_d(maxG, 16 * row));
-    }
+    // the largest objective over the wave (rows of 16 lanes by DPP, then the
+    // four rows), then the largest k that reaches it; both exact
+    double rm = best_r;
+#define DBW_MAX_STEP(CTRL) rm = fmax(rm, dpp_d<CTRL>(rm));
+    DBW_MAX_STEP(0xB1)
+    DBW_MAX_STEP(0x4E)
+    DBW_MAX_STEP(0x141)
+    DBW_MAX_STEP(0x140)
+#undef DBW_MAX_STEP
+    const double rmax = fmax(fmax(readlane_d(rm, 0), readlane_d(rm, 16)), fmax(readlane_d(rm, 32), readlane_d(rm, 48)));
+    int kc = best_k != 0 && best_r == rmax ? best_k : 0;
+#define DBW_KMAX_STEP(CTRL) kc = max(kc, dpp_i<CTRL>(kc));
+    DBW_KMAX_STEP(0xB1)
+    DBW_KMAX_STEP(0x4E)
+    DBW_KMAX_STEP(0x141)
+    DBW_KMAX_STEP(0x140)
+#undef DBW_KMAX_STEP
+    const int kb = max(max(__builtin_amdgcn_readlane(kc, 0), __builtin_amdgcn_readlane(kc, 16)),
+                       max(__builtin_amdgcn_readlane(kc, 32), __builtin_amdgcn_readlane(kc, 48)));
+    const bool all_negative = __builtin_amdgcn_ballot_w64(nonneg) == 0;
     if (lane == 0) {
-      int k = (!hasL || kb == 0 || g < 0.0) ? n : kb;
+      int k = (!hasL || kb == 0 || all_negative) ? n : kb;
       // loss guard: never decrease k while the loss estimate rises
       if (st.nF >= 2 && st.F_prev > a.beta * st.F_prev2 && st.k_prev < n) k = max(k, st.k_prev + 1);
       if (a.policy == DBW_POLICY_STATIC) k = a.k_static;
@@ -280,6 +290,73 @@ __device__ __forceinline__ int col_index(int lane, int q) {
   return VEC4 ? lane * 4 + q : lane + WAVE * q;
 }
 
+// Column of w (layout [d][C]) of element e of a slab partial; -1 for the
+// padding features of the tile order.  Tile order: 64-feature groups of 64C
+// floats; in a group, float4 piece (4 jq + g) C + m holds class m of features
+// 16 g + 4 t + jq, t = 0..3.
+// (Elements and columns fit 32 bits: a worker's partials are addressed by
+// one buffer descriptor, below 2^32 bytes.)
+template <int SRC>
+__device__ __forceinline__ int slab_column(const AggArgs& a, int e) {
+  if (e >= a.slab_len) return -1;
+  if (SRC == SRC_SLABS) return e < a.P ? e : -1;
+  const int C = a.C;
+  const int grp = e / (64 * C);
+  const int r = e - grp * 64 * C;
+  const int piece = r >> 2, t = r & 3;
+  const int m = piece % C, jg = piece / C;
+  const int f = 64 * grp + 16 * (jg & 3) + 4 * t + (jg >> 2);
+  return f < a.d ? f * C + m : -1;
+}
+
+// Columns of w of the lane's four elements e0 .. e0 + 3 (-1: padding or
+// past the partial) and the mask of those that are columns.  The same for
+// every row, so taken once.
+template <int SRC>
+__device__ __forceinline__ int slab_lane_cols(const AggArgs& a, int e0, int (&col)[4]) {
+  int m = 0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    col[t] = slab_column<SRC>(a, e0 + t);
+    if (col[t] >= 0) m |= 1 << t;
+  }
+  return m;
+}
+
+// Worker j's gradient at elements base + 4 lane .. + 3 of the slab layout:
+// the sum of its slab partials in slab order (the same additions as the slab
+// reduction); 0 for an invalid row and where vmask (slab_lane_mask) is clear.
+// S > 0: a.slabs == S, so every load is issued before the first addition.
+template <int SRC, int S>
+__device__ __forceinline__ void load_slab_row(const AggArgs& a, int j, int64_t base, int lane, float v[4],
+                                              bool valid, int vmask) {
+  // the descriptor depends on the row only (uniform per wave: no per-lane
+  // loop over descriptors); lanes outside vmask read in-range or zero
+  // values that are dropped below
+  const int64_t e0 = base + lane * 4;
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(a.Gp + (int64_t)(valid ? j : 0) * a.slabs * a.slab_len,
+                                             valid ? static_cast<uint32_t>(a.slabs * a.slab_len * 4) : 0u);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if constexpr (S > 0) {
+    float4 xs[S];
+#pragma unroll
+    for (int q = 0; q < S; ++q) xs[q] = buf_f32x4(r, static_cast<uint32_t>((q * a.slab_len + e0) * 4));
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+      acc.x += xs[q].x; acc.y += xs[q].y; acc.z += xs[q].z; acc.w += xs[q].w;
+    }
+  } else {
+    for (int q = 0; q < a.slabs; ++q) {
+      const float4 x = buf_f32x4(r, static_cast<uint32_t>((q * a.slab_len + e0) * 4));
+      acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
+    }
+  }
+  v[0] = vmask & 1 ? acc.x : 0.f;
+  v[1] = vmask & 2 ? acc.y : 0.f;
+  v[2] = vmask & 4 ? acc.z : 0.f;
+  v[3] = vmask & 8 ? acc.w : 0.f;
+}
+
 // LDS of one aggregation tile worked by NW waves.
 template <int NW>
 struct AggShared {
@@ -295,28 +372,42 @@ struct AggShared {
 // columns.
 constexpr int AGG_U = 4;
 
-// Loads of rows r0 + u NW (u < AGG_U) below rmax; jj = -1 past rmax.
-template <bool VEC4, int NW>
+// Loads of rows r0 + u NW (u < U) below rmax; jj = -1 past rmax.
+template <bool VEC4, int NW, int SRC = SRC_ROWS, int S = 0, int U = AGG_U>
 __device__ __forceinline__ void agg_load_round(const AggArgs& a, const int32_t* sel, int r0, int rmax,
-                                               float (&x)[AGG_U][4], int (&jj)[AGG_U]) {
+                                               float (&x)[U][4], int (&jj)[U], int vmask = 0) {
   const int lane = threadIdx.x % WAVE;
   const int64_t base = (int64_t)blockIdx.x * AGG_TILE;
 #pragma unroll
-  for (int u = 0; u < AGG_U; ++u) {
+  for (int u = 0; u < U; ++u) {
     const int r = r0 + u * NW;
-    jj[u] = r < rmax ? __builtin_amdgcn_readfirstlane(sel[r]) : -1;   // uniform per wave
-    load_tile<VEC4>(a.G + (int64_t)(jj[u] < 0 ? 0 : jj[u]) * a.P, base, lane, a.P, x[u], jj[u] >= 0);
+    // r is the same in every lane; taking the first lane's value makes the
+    // row, and so the buffer descriptor, provably uniform (no per-lane
+    // descriptor loop)
+    const int jv = r < rmax ? sel[r] : -1;
+    jj[u] = __builtin_amdgcn_readfirstlane(jv);
+    if (SRC == SRC_ROWS)
+      load_tile<VEC4>(a.G + (int64_t)(jj[u] < 0 ? 0 : jj[u]) * a.P, base, lane, a.P, x[u], jj[u] >= 0);
+    else
+      load_slab_row<SRC, S>(a, jj[u], base, lane, x[u], jj[u] >= 0, vmask);
   }
 }
 
-// Shifted sums of the loaded rows, and their squared norms.
-template <int MODE>
-__device__ __forceinline__ void agg_accumulate(const AggArgs& a, const float (&x)[AGG_U][4], const int (&jj)[AGG_U],
-                                               const float (&c)[4], float (&s1)[4], float (&s2)[4]) {
+// Shifted sums of the loaded rows, and their squared norms; from slab
+// partials, the rows are also stored in [d][C] order when G_rows is set.
+template <int MODE, int SRC = SRC_ROWS, int U = AGG_U>
+__device__ __forceinline__ void agg_accumulate(const AggArgs& a, const float (&x)[U][4], const int (&jj)[U],
+                                               const float (&c)[4], float (&s1)[4], float (&s2)[4],
+                                               int vmask = 0, const int* ocol = nullptr) {
   const int lane = threadIdx.x % WAVE;
 #pragma unroll
-  for (int u = 0; u < AGG_U; ++u) {
+  for (int u = 0; u < U; ++u) {
     if (jj[u] < 0) break;
+    if (SRC != SRC_ROWS && a.G_rows) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (vmask >> q & 1) a.G_rows[(int64_t)jj[u] * a.P + ocol[q]] = x[u][q];
+    }
     float sq = 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -334,7 +425,7 @@ __device__ __forceinline__ void agg_accumulate(const AggArgs& a, const float (&x
 
 // Column results from the waves' partial sums: g, the update, and the block
 // partials of the statistics.
-template <bool VEC4, int MODE, int NW>
+template <bool VEC4, int MODE, int NW, int SRC = SRC_ROWS>
 __device__ void agg_finish(const AggArgs& a, int k, const float (&c)[4], const float (&s1)[4], const float (&s2)[4],
                            AggShared<NW>& sh, const float* w_old = nullptr) {
   const int tid = threadIdx.x;
@@ -351,9 +442,12 @@ __device__ void agg_finish(const AggArgs& a, int k, const float (&c)[4], const f
   __syncthreads();
 
   const int64_t col = base + tid;
+  // slab layouts: the element's column of w (-1 at padding, whose sums are 0)
+  const int64_t out = SRC == SRC_ROWS ? col : slab_column<SRC>(a, static_cast<int>(col));
+  const int64_t ncol = SRC == SRC_ROWS ? P : a.slab_len;
   const float kf = static_cast<float>(k);
   double m2 = 0.0, g2 = 0.0;
-  if (tid < AGG_TILE && col < P) {
+  if (tid < AGG_TILE && col < ncol) {
     float S1 = 0.f, S2 = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
@@ -367,31 +461,54 @@ __device__ void agg_finish(const AggArgs& a, int k, const float (&c)[4], const f
       m2 = S2;
     } else {
       g = cs + S1 / kf;
-      a.g_out[col] = g;
+      if (out >= 0) a.g_out[out] = g;
       if (MODE == AGG_FUSED) {
         m2 = S2 - S1 * S1 / kf;
-        if (a.w) a.w[col] = (w_old ? *w_old : a.w[col]) - a.eta * g;
+        if (a.w && out >= 0) a.w[out] = (w_old ? *w_old : a.w[out]) - a.eta * g;
       }
     }
     g2 = static_cast<double>(g) * g;
   }
   if (MODE != AGG_MEAN) {
-    double v[2] = {m2, g2};
-    block_sums_d<2>(v, sh.red);
+    // the tile's sums: the AGG_TILE column threads fill the first waves;
+    // a DPP tree in each, then those waves' sums in order
+    constexpr int TW = AGG_TILE / WAVE;
+    if (wv < TW) {
+      m2 = row_sum_d(m2);
+      g2 = row_sum_d(g2);
+      // the four row sums are read with the whole wave active (a read
+      // inside the lane-0 branch would let the compiler compute the other
+      // rows' sums there, for lane 0 only)
+      const double wm2 = readlane_d(m2, 0) + readlane_d(m2, 16) + readlane_d(m2, 32) + readlane_d(m2, 48);
+      const double wg2 = readlane_d(g2, 0) + readlane_d(g2, 16) + readlane_d(g2, 32) + readlane_d(g2, 48);
+      if (lane == 0) {
+        sh.red[wv] = wm2;
+        sh.red[TW + wv] = wg2;
+      }
+    }
+    __syncthreads();
     if (tid == 0) {
-      a.part[blk * 2 + 0] = v[0];
-      a.part[blk * 2 + 1] = v[1];
+      double s0 = sh.red[0], s1v = sh.red[TW];
+#pragma unroll
+      for (int w = 1; w < TW; ++w) {
+        s0 += sh.red[w];
+        s1v += sh.red[TW + w];
+      }
+      a.part[blk * 2 + 0] = s0;
+      a.part[blk * 2 + 1] = s1v;
     }
   }
 }
 
 // The shift row's tile: the mean itself (given) or the fastest worker's row.
-template <bool VEC4, int MODE>
-__device__ __forceinline__ void agg_shift(const AggArgs& a, const int32_t* sel, float (&c)[4]) {
+template <bool VEC4, int MODE, int SRC = SRC_ROWS, int S = 0>
+__device__ __forceinline__ void agg_shift(const AggArgs& a, const int32_t* sel, float (&c)[4], int vmask = 0) {
   const int lane = threadIdx.x % WAVE;
   const int64_t base = (int64_t)blockIdx.x * AGG_TILE;
   if (MODE == AGG_STATS_GIVEN_MEAN) load_tile<VEC4>(a.g_in, base, lane, a.P, c);
-  else load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(sel[0]) * a.P, base, lane, a.P, c);
+  else if (SRC == SRC_ROWS)
+    load_tile<VEC4>(a.G + (int64_t)__builtin_amdgcn_readfirstlane(sel[0]) * a.P, base, lane, a.P, c);
+  else load_slab_row<SRC, S>(a, __builtin_amdgcn_readfirstlane(sel[0]), base, lane, c, true, vmask);
 }
 
 template <bool VEC4, int MODE, int NW>
@@ -421,10 +538,16 @@ __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
 // so every block reaches the same k), takes the first k_t workers of the
 // arrival order the host sorted (ties to the lower index), and aggregates its
 // column tile with the SGD update; block 0 also stores the choice, the
-// selection and the device copies of T_hat and the ticks.
-template <bool VEC4>
+// selection and the device copies of T_hat and the ticks.  With a slab
+// source the rows are the selected workers' slab partials summed in place
+// (tiles follow the partial's layout, results land at their [d][C] column),
+// and block 0 also turns every worker's slab loss sums into its loss.
+template <bool VEC4, int SRC = SRC_ROWS, int S = 0>
 __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca, AggArgs a) {
   constexpr int NW = STEP_PS_WAVES;
+  // rows per wave and round: about 8 float4 loads in flight per lane within
+  // the 128 registers a 16-wave block leaves each wave
+  constexpr int RU = SRC == SRC_ROWS ? AGG_U : S > 0 ? (8 / S > 1 ? 8 / S : 1) : 2;
   __shared__ ChooseShared cs;
   __shared__ AggShared<NW> sh;
   __shared__ int32_t sh_order[DBW_MAX_N];
@@ -436,7 +559,9 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
   // every host and device read of the prologue is issued before any use
   load_state(ca.st, &cs.st);
   const int64_t col = (int64_t)blockIdx.x * AGG_TILE + tid;
-  const float w_old = tid < AGG_TILE && col < a.P && a.w ? a.w[col] : 0.f;
+  int64_t wcol = col < a.P ? col : -1;
+  if (SRC != SRC_ROWS) wcol = slab_column<SRC>(a, static_cast<int>(col));
+  const float w_old = tid < AGG_TILE && wcol >= 0 && a.w ? a.w[wcol] : 0.f;
   for (int i = tid; i < n; i += blockDim.x) {
     const double T = ca.T_src[i];
     const int32_t o = ca.order_src[i];
@@ -452,13 +577,22 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
   __syncthreads();
   // the first rows of the arrival order are loaded while the choice runs
   // (k_t >= 1 rows are needed; rows past k_t are dropped)
+  int ocol[4];
+  const int vmask = SRC == SRC_ROWS ? 0 : slab_lane_cols<SRC>(a, static_cast<int>(blockIdx.x) * AGG_TILE + lane * 4, ocol);
   float c[4];
-  agg_shift<VEC4, AGG_FUSED>(a, sh_order, c);
-  float x[AGG_U][4];
-  int jj[AGG_U];
-  agg_load_round<VEC4, NW>(a, sh_order, wv, n, x, jj);
+  agg_shift<VEC4, AGG_FUSED, SRC, S>(a, sh_order, c, vmask);
+  float x[RU][4];
+  int jj[RU];
+  agg_load_round<VEC4, NW, SRC, S, RU>(a, sh_order, wv, n, x, jj, vmask);
   choose_k(ca, cs, lead);
   const int k = cs.kfinal;
+  if (SRC != SRC_ROWS && lead) {
+    for (int i = tid; i < n; i += blockDim.x) {
+      float l = 0.f;
+      for (int q = 0; q < a.slabs; ++q) l += a.lossp[(int64_t)i * a.slabs + q];
+      a.loss[i] = l / static_cast<float>(a.B);
+    }
+  }
   if (lead) {
     int finite = 0;
     for (int r = tid; r < n; r += blockDim.x) {
@@ -479,15 +613,15 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
     }
   }
 #pragma unroll
-  for (int u = 0; u < AGG_U; ++u)
+  for (int u = 0; u < RU; ++u)
     if (wv + u * NW >= k) jj[u] = -1;
   float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
-  agg_accumulate<AGG_FUSED>(a, x, jj, c, s1, s2);
-  for (int r0 = wv + NW * AGG_U; r0 < k; r0 += NW * AGG_U) {
-    agg_load_round<VEC4, NW>(a, sh_order, r0, k, x, jj);
-    agg_accumulate<AGG_FUSED>(a, x, jj, c, s1, s2);
+  agg_accumulate<AGG_FUSED, SRC, RU>(a, x, jj, c, s1, s2, vmask, ocol);
+  for (int r0 = wv + NW * RU; r0 < k; r0 += NW * RU) {
+    agg_load_round<VEC4, NW, SRC, S, RU>(a, sh_order, r0, k, x, jj, vmask);
+    agg_accumulate<AGG_FUSED, SRC, RU>(a, x, jj, c, s1, s2, vmask, ocol);
   }
-  agg_finish<VEC4, AGG_FUSED, NW>(a, k, c, s1, s2, sh, &w_old);
+  agg_finish<VEC4, AGG_FUSED, NW, SRC>(a, k, c, s1, s2, sh, &w_old);
 }
 
 // ---------------------------------------------------------------------------
@@ -618,9 +752,34 @@ hipError_t launch_aggregate(const AggArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int SRC>
+void launch_step_ps_slabs(const ChooseArgs& ca, const AggArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  switch (a.slabs) {
+#define DBW_SLABS_CASE(S) \
+    case S: hipLaunchKernelGGL((k_step_ps<true, SRC, S>), grid, block, 0, s, ca, a); return;
+    DBW_SLABS_CASE(2)
+    DBW_SLABS_CASE(3)
+    DBW_SLABS_CASE(4)
+    DBW_SLABS_CASE(5)
+    DBW_SLABS_CASE(6)
+    DBW_SLABS_CASE(7)
+    DBW_SLABS_CASE(8)
+#undef DBW_SLABS_CASE
+    default: hipLaunchKernelGGL((k_step_ps<true, SRC, 0>), grid, block, 0, s, ca, a);
+  }
+}
+
 hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
   const dim3 block(STEP_PS_WAVES * WAVE);
+  if (a.src != SRC_ROWS) {
+    // slab partials: float4 pieces of 4 consecutive elements
+    if (a.slab_len % 4 != 0 || !a.Gp || !a.lossp || !a.loss || a.slabs < 1) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(agg_blocks(a.slab_len)));
+    if (a.src == SRC_SLAB_TILES) launch_step_ps_slabs<SRC_SLAB_TILES>(ca, a, grid, block, s);
+    else launch_step_ps_slabs<SRC_SLABS>(ca, a, grid, block, s);
+    return hipGetLastError();
+  }
+  const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
   if ((a.P % 4) == 0) hipLaunchKernelGGL(k_step_ps<true>, grid, block, 0, s, ca, a);
   else hipLaunchKernelGGL(k_step_ps<false>, grid, block, 0, s, ca, a);
   return hipGetLastError();

@@ -931,7 +931,7 @@ hipError_t launch_fused_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_
   hipLaunchKernelGGL((k_softmax_fused<CP, M, T, R>), dim3(static_cast<unsigned>(per_xcd * NXCD)), dim3(T), 0, s,
                      a, p.slabs, p.rows_per_slab, per_xcd);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.slabs == 1) return e;
+  if (e != hipSuccess || p.slabs == 1 || a.keep_slabs) return e;
   const int64_t P = (int64_t)a.d * a.C;
   const dim3 g2(static_cast<unsigned>((P + 1023) / 1024), static_cast<unsigned>(a.n));
   hipLaunchKernelGGL(k_slab_reduce, g2, dim3(256), 0, s, a, p.slabs);
@@ -945,7 +945,7 @@ hipError_t launch_mfma_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t
   hipLaunchKernelGGL((k_softmax_mfma<U, CW>), dim3(static_cast<unsigned>(per_xcd * NXCD)), dim3(MF_T), 0, s, a,
                      p.slabs, p.rows_per_slab, per_xcd);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.slabs == 1) return e;
+  if (e != hipSuccess || p.slabs == 1 || a.keep_slabs) return e;
   const dim3 g2(static_cast<unsigned>((a.d + 63) / 64), static_cast<unsigned>(a.n));
   hipLaunchKernelGGL(k_slab_reduce_tiles, g2, dim3(256), 0, s, a, p.slabs, U);
   return hipGetLastError();

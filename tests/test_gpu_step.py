@@ -54,7 +54,12 @@ def _compare_iteration(cfg, rec, out, k_gpu, w_prev32, w_new, st_before, st_afte
             if v is not None:
                 assert obj[kk] == pytest.approx(v, rel=1e-9, abs=1e-300), (tag, kk)
     Gg = host(out["G"])
-    for i in range(n):
+    # with g_rows "selected" only the selected workers' rows are written
+    if cfg.g_rows == "all":
+        check_rows = range(n)
+    else:
+        check_rows = rec["sel"] if k_gpu == rec["k"] else []
+    for i in check_rows:
         assert masked_rel_err(Gg[i], rec["G"][i], masks[i]) <= RTOL, (tag, i)
     assert rel_err(host(out["loss"]), rec["loss"]) <= RTOL, tag
     if k_gpu != rec["k"]:
@@ -246,6 +251,55 @@ def test_free_running_trajectory(cfg):
         out = ctx.step_outputs()
         assert scalar_rel(host(out["stats"])[3], rec["F_hat"]) <= 1e-3, t
     assert rel_err(host(wd), orc.w) <= 1e-3
+
+
+def test_lockstep_selected_rows_16_workers():
+    # the selected workers' slab partials are aggregated in one kernel; only
+    # their rows of G are written
+    _lockstep(C2.replace(g_rows="selected"), 60)
+
+
+def test_lockstep_selected_rows_64_workers_first_iterations():
+    _lockstep(C3.replace(g_rows="selected"), 8)
+
+
+@pytest.mark.parametrize("base", [C2, C3], ids=lambda c: c.name)
+def test_slab_aggregation_matches_row_aggregation(base):
+    # The same iterations with every row of G written and read back, with the
+    # selected rows only, and with none: k, the mask, g, the update and the
+    # losses are bitwise equal; the statistics differ only by the order of
+    # their partial sums.  Rows of workers that were not selected keep stale
+    # values in the fused modes.
+    cfg = base.replace(policy="static", k_static=base.n // 2 + 1)
+    X, y = gen.dataset(cfg)
+    Xd, yd = to_dev(torch, X), to_dev(torch, y)
+    modes = ("all", "selected", "none")
+    ctxs = {m: pb.Context(pb.config_from(cfg.replace(g_rows=m), S=cfg.S)) for m in modes}
+    ws = {m: to_dev(torch, init_params(cfg)) for m in modes}
+    stale = 0
+    for t in range(4):
+        rows = to_dev(torch, gen.batch_indices(cfg, t))
+        ticks = gen.round_trip_ticks(cfg, t)
+        ks = {m: ctxs[m].step(ws[m], Xd, yd, ticks, rows=rows, wait=True) for m in modes}
+        outs = {m: {k: host(v) for k, v in ctxs[m].step_outputs().items()} for m in modes}
+        for m in modes:
+            ctxs[m].sync()
+        ref = outs["all"]
+        assert ks["selected"] == ks["none"] == ks["all"] == cfg.k_static, t
+        sel = np.flatnonzero(ref["mask"])
+        for m in ("selected", "none"):
+            o = outs[m]
+            for name in ("mask", "g", "loss", "k", "b", "T_hat"):
+                assert np.array_equal(o[name], ref[name], equal_nan=True), (m, t, name)
+            assert np.array_equal(host(ws[m]), host(ws["all"])), (m, t)
+            assert np.array_equal(o["stats"][3], ref["stats"][3]), (m, t)       # F_hat: same losses
+            np.testing.assert_allclose(o["stats"], ref["stats"], rtol=1e-12, atol=0)
+            np.testing.assert_allclose(o["sqnorm"], ref["sqnorm"], rtol=1e-5, atol=0)
+        Gs, Ga = outs["selected"]["G"], ref["G"]
+        assert np.array_equal(Gs[sel], Ga[sel]), t
+        unsel = np.setdiff1d(np.arange(cfg.n), sel)
+        stale += sum(not np.array_equal(Gs[j], Ga[j]) for j in unsel)
+    assert stale > 0
 
 
 def test_step_is_bitwise_deterministic():
