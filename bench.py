@@ -138,7 +138,7 @@ def main(argv=None) -> int:
     ap.add_argument("--k-static", type=int, default=0)
     ap.add_argument("--estimator", choices=("isotonic", "naive"), default="isotonic",
                     help="time estimate: constrained least squares, or the mean of cell (k,k)")
-    ap.add_argument("--g-rows", choices=("all", "selected", "none"), default="all",
+    ap.add_argument("--g-rows", choices=("all", "selected", "none"), default="none",
                     help="worker-gradient rows a step writes; with selected/none the selected "
                          "workers' slab partials are aggregated in one kernel where the softmax "
                          "kernel splits rows into slabs")

@@ -96,7 +96,7 @@ struct dbw_ctx {
   int32_t* d_order = nullptr;
   int32_t* d_k = nullptr;
   int32_t* h_err = nullptr;     // [1]
-  hipEvent_t ev_k[kSlots]{};    // after the slot's PS kernel: k is in h_k
+  hipEvent_t ev_k[kSlots]{};    // (unused by dbw_step: k is polled in h_k)
 
   // host bookkeeping of arrival times
   int64_t t = 0;                // next iteration index (== device state t once drained)
@@ -214,9 +214,29 @@ dbw_status known_k(dbw_ctx* c, int64_t u, int32_t* k) {
     }
     return fail(c, DBW_ESTATE, "iteration %lld precedes the context's history", (long long)u);
   }
+  // the PS kernel of u writes k_u into its pinned slot (0 until then) early
+  // in its run; polling it keeps an event out of the stream and lets the
+  // host go on before the kernel ends.  Seeing it also proves the stream has
+  // finished every earlier kernel.  A HIP error, or a stream that drained
+  // without the value, ends the wait.
   const int slot = static_cast<int>(u % kSlots);
-  HIP_TRY(c, hipEventSynchronize(c->ev_k[slot]));
-  *k = c->h_k[slot];
+  for (int64_t spin = 0;; ++spin) {
+    const int32_t v = __atomic_load_n(c->h_k + slot, __ATOMIC_ACQUIRE);
+    if (v != 0) {
+      *k = v;
+      break;
+    }
+    if (spin % 4096 == 4095) {
+      const hipError_t q = hipStreamQuery(c->stream);
+      if (q == hipSuccess && __atomic_load_n(c->h_k + slot, __ATOMIC_ACQUIRE) == 0)
+        return fail(c, DBW_ESTATE, "choice of iteration %lld did not complete", (long long)u);
+      if (q != hipSuccess && q != hipErrorNotReady)
+        return fail(c, DBW_EHIP, "waiting for the choice of iteration %lld: %s", (long long)u, hipGetErrorString(q));
+      std::this_thread::yield();
+    } else {
+      __builtin_ia32_pause();
+    }
+  }
   if (*k < 1 || *k > c->cfg.n)
     return fail(c, DBW_ESTATE, "choice of iteration %lld did not complete (k=%d)", (long long)u, *k);
   return DBW_OK;
@@ -556,6 +576,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   ok = ok && hipHostGetDevicePointer((void**)&c->d_ticks, c->h_ticks, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_order, c->h_order, 0) == hipSuccess;
   ok = ok && hipHostGetDevicePointer((void**)&c->d_k, c->h_k, 0) == hipSuccess;
+  if (ok) std::memset(c->h_k, 0, sizeof(int32_t) * kSlots);
   ok = ok && hipHostMalloc((void**)&c->h_err, sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_fin, hipEventDisableTiming) == hipSuccess;
   for (int s = 0; s < kSlots && ok; ++s) {
@@ -770,6 +791,9 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   //    run beside it)
   {
     ProfScope ps(c, DBW_KT_AGGREGATE);
+    // k_t's pinned slot reads 0 until the PS kernel writes k_t (its previous
+    // value, k_{t-4}, was read before the estimate of t-2)
+    __atomic_store_n(c->h_k + slot, 0, __ATOMIC_RELEASE);
     dbw::ChooseArgs ca{};
     ca.st = c->st; ca.T_src = c->d_T + (size_t)slot * n; ca.ticks_src = c->d_ticks + (size_t)slot * n;
     ca.order_src = c->d_order + (size_t)slot * n;
@@ -794,7 +818,6 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     } else {
       HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
     }
-    HIP_TRY(c, hipEventRecord(c->ev_k[slot], c->stream));
     if (!fused) HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
     // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored
     // above, and k_{t-1}); the rest of the queueing overlaps its solve
