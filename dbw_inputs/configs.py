@@ -18,6 +18,7 @@ from typing import Optional, Tuple
 
 SOFTMAX = "softmax"
 MLP = "mlp"
+CNN = "cnn"     # 28x28 images: conv 5x5 (20) - pool - conv 5x5 (50) - pool - FC H - FC C
 
 # Round trip times are kept as integer ticks of 2**-20 time units, so that
 # sums of samples and their order are exact on every side.
@@ -84,6 +85,8 @@ class DBWConfig:
         [W1 (d x H) | b1 (H) | W2 (H x C) | b2 (C)]."""
         if self.model == SOFTMAX:
             return self.d * self.C
+        if self.model == CNN:
+            return 20 * 25 + 20 + 50 * 20 * 25 + 50 + 800 * self.H + self.H + self.H * self.C + self.C
         return self.d * self.H + self.H + self.H * self.C + self.C
 
     def replace(self, **kw) -> "DBWConfig":
@@ -119,7 +122,16 @@ C5 = DBWConfig(
                     straggler_prob=0.1, straggler_factor=10.0),
 )
 
-CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5)}
+# The paper's MNIST network shape (two 5x5 convolutions, two fully connected
+# layers), its MNIST setting n = 16, B = 500, eta = 0.01, round trips
+# 0.3 + 0.7 Exp(1); 28x28 synthetic images with MNIST-like sparsity.
+C6 = DBWConfig(
+    name="C6", model=CNN, n=16, B=500, d=784, C=10, H=500, S=60000, iters=20, eta=0.01,
+    features="uniform", sparsity=0.8, seed=14696 + 6,
+    times=TimeModel(kind="shifted_exp", shift=0.3, rate=1.0 / 0.7),
+)
+
+CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5, C6)}
 
 
 def get(name: str) -> DBWConfig:
@@ -129,5 +141,5 @@ def get(name: str) -> DBWConfig:
 def describe(cfg: DBWConfig) -> str:
     tm = cfg.times
     return (f"{cfg.name}: {cfg.model} n={cfg.n} B={cfg.B} d={cfg.d} C={cfg.C}"
-            + (f" H={cfg.H}" if cfg.model == MLP else "")
+            + (f" H={cfg.H}" if cfg.model in (MLP, CNN) else "")
             + f" S={cfg.S} P={cfg.param_count} iters={cfg.iters} times={tm.kind}")

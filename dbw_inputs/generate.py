@@ -16,7 +16,7 @@ import functools
 
 import numpy as np
 
-from .configs import MLP, SOFTMAX, TICKS_PER_UNIT, DBWConfig
+from .configs import CNN, MLP, SOFTMAX, TICKS_PER_UNIT, DBWConfig
 
 STREAM_FEATURES, STREAM_LABELS, STREAM_INIT, STREAM_INDICES, STREAM_TIMES = range(5)
 
@@ -64,6 +64,15 @@ def init_params(cfg: DBWConfig) -> np.ndarray:
         W2 = r.normal(0.0, np.sqrt(2.0 / cfg.H), size=(cfg.H, cfg.C)).astype(np.float32)
         return np.concatenate([W1.ravel(), np.zeros(cfg.H, np.float32),
                                W2.ravel(), np.zeros(cfg.C, np.float32)])
+    if cfg.model == CNN:
+        # PyTorch's default for convolution and linear layers: weights and
+        # biases uniform in +-1/sqrt(fan_in)
+        parts = []
+        for shape, fan_in in (((20, 1, 5, 5), 25), ((20,), 25), ((50, 20, 5, 5), 500), ((50,), 500),
+                              ((800, cfg.H), 800), ((cfg.H,), 800), ((cfg.H, cfg.C), cfg.H), ((cfg.C,), cfg.H)):
+            bound = 1.0 / np.sqrt(fan_in)
+            parts.append(r.uniform(-bound, bound, size=shape).astype(np.float32).ravel())
+        return np.concatenate(parts)
     raise ValueError(cfg.model)
 
 

@@ -144,3 +144,107 @@ def test_full_sync_equals_union_batch(which):
     g = ps.aggregate(G, list(range(n)))
     np.testing.assert_allclose(g, Gu[0], rtol=1e-12, atol=1e-15)
     assert np.mean(loss) == pytest.approx(lu[0], rel=1e-12)
+
+
+# -- the CNN -----------------------------------------------------------------
+
+def _cnn_torch(w, X, y, H, C, torch):
+    """The network from its layer definitions in torch (float64, CPU)."""
+    F = torch.nn.functional
+    sizes = [(20, 1, 5, 5), (20,), (50, 20, 5, 5), (50,), (800, H), (H,), (H, C), (C,)]
+    ps_, o = [], 0
+    for sh in sizes:
+        m = int(np.prod(sh))
+        ps_.append(torch.tensor(w[o:o + m].reshape(sh), requires_grad=True))
+        o += m
+    Wc1, bc1, Wc2, bc2, Wf1, bf1, Wf2, bf2 = ps_
+    x = torch.tensor(X.reshape(-1, 1, 28, 28))
+    a = F.relu(F.max_pool2d(F.conv2d(x, Wc1, bc1), 2))
+    a = F.relu(F.max_pool2d(F.conv2d(a, Wc2, bc2), 2))
+    a = F.relu(a.reshape(-1, 800) @ Wf1 + bf1)
+    L = F.cross_entropy(a @ Wf2 + bf2, torch.tensor(y))
+    L.backward()
+    return np.concatenate([p.grad.numpy().ravel() for p in ps_]), L.item()
+
+
+def test_cnn_matches_autograd():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(61)
+    n, B, H, C = 2, 5, 24, 10
+    Xt = np.where(rng.random((n, B, 784)) < 0.7, 0.0, rng.random((n, B, 784)))
+    yt = rng.integers(0, C, size=(n, B))
+    w = rng.uniform(-0.3, 0.3, size=model.cnn_param_count(H, C))
+    G, loss = model.cnn_worker_grads(w, Xt, yt, H, C)
+    for i in range(n):
+        ref, L = _cnn_torch(w, Xt[i], yt[i], H, C, torch)
+        np.testing.assert_allclose(G[i], ref, rtol=1e-10, atol=1e-13)
+        assert loss[i] == pytest.approx(L, rel=1e-12)
+
+
+def test_cnn_finite_differences():
+    # a few parameters of every block, one worker of three images
+    rng = np.random.default_rng(62)
+    B, H, C = 3, 8, 4
+    X = rng.random((1, B, 784))
+    y = rng.integers(0, C, size=(1, B))
+    w = rng.uniform(-0.15, 0.15, size=model.cnn_param_count(H, C))
+    G, L0 = model.cnn_worker_grads(w, X, y, H, C)
+
+    def loss_at(v):
+        return model.cnn_worker_grads(v, X, y, H, C)[1][0]
+
+    bounds = np.cumsum([0, 500, 20, 25000, 50, 800 * H, H, H * C, C])
+    h = 1e-5      # the loss is ~1: smaller steps drown gradients of ~1e-7 in rounding
+    for lo, hi in zip(bounds[:-1], bounds[1:]):
+        for p in rng.choice(np.arange(lo, hi), size=min(4, hi - lo), replace=False):
+            e = np.zeros_like(w)
+            e[p] = h
+            fd = (loss_at(w + e) - loss_at(w - e)) / (2 * h)
+            # rounding of the two losses: about eps |loss| / h
+            assert G[0, p] == pytest.approx(fd, rel=1e-4, abs=50 * 2.2e-16 * L0[0] / h), (lo, p)
+
+
+def test_cnn_closed_form_at_zero():
+    # all parameters 0: logits 0, uniform class probabilities, loss ln C; only
+    # the last bias has a gradient, the batch mean of 1/C - onehot(y)
+    B, H, C = 6, 10, 5
+    y = np.array([[0, 1, 1, 4, 2, 1]])
+    X = np.random.default_rng(63).random((1, B, 784))
+    G, loss = model.cnn_worker_grads(np.zeros(model.cnn_param_count(H, C)), X, y, H, C)
+    expect = np.zeros(model.cnn_param_count(H, C))
+    expect[-C:] = [(1 / C) - np.mean(y[0] == c) for c in range(C)]
+    np.testing.assert_allclose(G[0], expect, rtol=0, atol=1e-15)
+    assert loss[0] == pytest.approx(np.log(C), rel=1e-14)
+
+
+def test_convolution_and_its_input_gradient_by_loops():
+    rng = np.random.default_rng(64)
+    B, Ci, h, wd, Co, k = 2, 3, 6, 7, 4, 3
+    X = rng.normal(size=(B, Ci, h, wd))
+    W = rng.normal(size=(Co, Ci, k, k))
+    b = rng.normal(size=Co)
+    out, _ = model.conv_valid(X, W, b)
+    dOut = rng.normal(size=out.shape)
+    ref = np.zeros_like(out)
+    dX = np.zeros_like(X)
+    for bb in range(B):
+        for o in range(Co):
+            for y in range(h - k + 1):
+                for x in range(wd - k + 1):
+                    ref[bb, o, y, x] = b[o] + sum(X[bb, c, y + u, x + v] * W[o, c, u, v]
+                                                  for c in range(Ci) for u in range(k) for v in range(k))
+                    for c in range(Ci):
+                        for u in range(k):
+                            for v in range(k):
+                                dX[bb, c, y + u, x + v] += dOut[bb, o, y, x] * W[o, c, u, v]
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(model.conv_input_grad(dOut, W, h, wd), dX, rtol=1e-12, atol=1e-12)
+
+
+def test_pooling_passes_the_first_of_equal_values():
+    Z = np.array([[[[1.0, 3.0, 2.0, 2.0],
+                    [3.0, 0.0, 2.0, 2.0]]]])           # windows: (1,3,3,0) and (2,2,2,2)
+    P, code = model.maxpool2(Z)
+    assert P.tolist() == [[[[3.0, 2.0]]]] and code.tolist() == [[[[1, 0]]]]
+    dZ = model.maxpool2_grad(np.array([[[[5.0, 7.0]]]]), code)
+    assert dZ.tolist() == [[[[0.0, 5.0, 7.0, 0.0], [0.0, 0.0, 0.0, 0.0]]]]
