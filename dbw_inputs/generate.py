@@ -68,8 +68,9 @@ def init_params(cfg: DBWConfig) -> np.ndarray:
         # PyTorch's default for convolution and linear layers: weights and
         # biases uniform in +-1/sqrt(fan_in)
         parts = []
-        for shape, fan_in in (((20, 1, 5, 5), 25), ((20,), 25), ((50, 20, 5, 5), 500), ((50,), 500),
-                              ((800, cfg.H), 800), ((cfg.H,), 800), ((cfg.H, cfg.C), cfg.H), ((cfg.C,), cfg.H)):
+        # layout: the fully connected layers first, then the convolutions
+        for shape, fan_in in (((800, cfg.H), 800), ((cfg.H,), 800), ((cfg.H, cfg.C), cfg.H), ((cfg.C,), cfg.H),
+                              ((20, 1, 5, 5), 25), ((20,), 25), ((50, 20, 5, 5), 500), ((50,), 500)):
             bound = 1.0 / np.sqrt(fan_in)
             parts.append(r.uniform(-bound, bound, size=shape).astype(np.float32).ravel())
         return np.concatenate(parts)

@@ -21,7 +21,9 @@
  *   - Arrays are dense and row-major; float is IEEE fp32, double fp64.
  *   - Model parameters w have P = dbw_param_count(cfg) floats:
  *       softmax regression: W [d][C] (no bias), P = d*C;
- *       MLP d-H-C with ReLU: [W1 (d x H) | b1 (H) | W2 (H x C) | b2 (C)].
+ *       MLP d-H-C with ReLU: [W1 (d x H) | b1 (H) | W2 (H x C) | b2 (C)];
+ *       CNN: [W1 (800 x H) | b1 (H) | W2 (H x C) | b2 (C) | Wc1 (20 x 1 x 5 x 5) |
+ *       bc1 (20) | Wc2 (50 x 20 x 5 x 5) | bc2 (50)], P = 800 H + H + H C + C + 25570.
  *     Gradients use the same layout.
  *   - Every call returns a dbw_status; nothing throws across the ABI.  Argument
  *     errors are detected on the host before any work is queued (DBW_EINVAL,
@@ -51,7 +53,13 @@ typedef enum {
   DBW_EUNSUPPORTED = -5 /* shape the kernels do not handle                   */
 } dbw_status;
 
-typedef enum { DBW_SOFTMAX = 0, DBW_MLP = 1 } dbw_model;
+/* DBW_CNN: the MNIST network shape of Sect. 4 (two 5 x 5 convolutions and
+ * two fully connected layers) on 28 x 28 single-channel images (d = 784):
+ * conv 1 -> 20 channels, 2 x 2 max pooling, ReLU, conv 20 -> 50, 2 x 2 max
+ * pooling, ReLU, the 800 features (channel, row, column), FC 800 -> H with
+ * ReLU, FC H -> C.  Convolutions are valid, stride 1; a pooling window passes
+ * (and back-propagates to) its first largest entry in row-major order. */
+typedef enum { DBW_SOFTMAX = 0, DBW_MLP = 1, DBW_CNN = 2 } dbw_model;
 
 /* Virtual clock of the simulated cluster (Sect. 2, the synchronisation
  * variants; Sect. 3.2).  FRESH: every worker starts each iteration at its
@@ -151,7 +159,8 @@ int64_t dbw_param_count(const dbw_config* cfg);
 
 /* Create a context bound to HIP stream `stream` (a hipStream_t, NULL for the
  * default stream) on the current device.  Validates cfg (n in [1, DBW_MAX_N],
- * B, d, C >= 1, C <= 4096, H >= 1 for the MLP, D in [1, DBW_MAX_D], eta > 0,
+ * B, d, C >= 1, C <= 4096, H >= 1 for the MLP and the CNN, d = 784 for the
+ * CNN, D in [1, DBW_MAX_D], eta > 0,
  * beta >= 1, S >= 0), allocates all device workspace (no allocation happens in
  * later calls) and sets the estimator state to its initial value.  Returns
  * DBW_EUNSUPPORTED when one array the kernels address (P floats, the n*B*d

@@ -21,8 +21,9 @@ Parameter layouts (readings of an unspecified layout):
   out[o][y][x] = b[o] + sum_{c,u,v} in[c][y+u][x+v] W[o][c][u][v].  A pooling
   window passes its largest value; among equal values the first in
   row-major order of the window, which also receives the gradient.  Flat
-  [Wc1 (20x1x5x5) | bc1 | Wc2 (50x20x5x5) | bc2 | Wf1 (800 x H) | bf1 |
-  Wf2 (H x C) | bf2]: the fully connected part is laid out like the MLP.
+  [Wf1 (800 x H) | bf1 | Wf2 (H x C) | bf2 | Wc1 (20x1x5x5) | bc1 |
+  Wc2 (50x20x5x5) | bc2]: the fully connected part first, laid out like
+  the MLP.
 
 Test infrastructure only (see the package docstring).
 """
@@ -122,15 +123,16 @@ def cnn_param_count(H: int, C: int) -> int:
 def cnn_split(w: np.ndarray, H: int, C: int):
     w = np.asarray(w, dtype=np.float64)
     k = CNN_K
-    shapes = [(CNN_C1, 1, k, k), (CNN_C1,), (CNN_C2, CNN_C1, k, k), (CNN_C2,),
-              (CNN_FEAT, H), (H,), (H, C), (C,)]
+    shapes = [(CNN_FEAT, H), (H,), (H, C), (C,),
+              (CNN_C1, 1, k, k), (CNN_C1,), (CNN_C2, CNN_C1, k, k), (CNN_C2,)]
     out, o = [], 0
     for sh in shapes:
         m = int(np.prod(sh))
         out.append(w[o:o + m].reshape(sh))
         o += m
     assert o == w.size, "parameter vector length does not match the CNN"
-    return out
+    Wf1, bf1, Wf2, bf2, Wc1, bc1, Wc2, bc2 = out
+    return Wc1, bc1, Wc2, bc2, Wf1, bf1, Wf2, bf2
 
 
 def im2col(X: np.ndarray, k: int) -> np.ndarray:
@@ -194,14 +196,16 @@ def maxpool2_grad(dP: np.ndarray, code: np.ndarray):
 def cnn_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: int,
                      return_preact: bool = False):
     """The CNN above.  Xt [n][B][784] (row-major 28 x 28 images).  Returns
-    G [n][P] flattened like w, loss [n] and, on request, the first fully
-    connected layer's pre-activations [n][B][H] (its ReLU decisions)."""
+    G [n][P] flattened like w, loss [n] and, on request, per worker the
+    values its decisions were taken on: {"Z1": conv1 outputs [B][20][24][24],
+    "Z2": conv2 outputs [B][50][8][8], "A3": first fully connected layer's
+    pre-activations [B][H]}."""
     n, B, d = Xt.shape
     assert d == CNN_IMG * CNN_IMG
     Wc1, bc1, Wc2, bc2, Wf1, bf1, Wf2, bf2 = cnn_split(w, H, C)
     G = np.empty((n, w.size))
     loss = np.empty(n)
-    A_all = np.empty((n, B, H)) if return_preact else None
+    dec = [] if return_preact else None
     for i in range(n):
         X = np.asarray(Xt[i], dtype=np.float64).reshape(B, 1, CNN_IMG, CNN_IMG)
         y = np.asarray(yt[i], dtype=np.int64)
@@ -230,13 +234,13 @@ def cnn_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: i
         dZ1 = maxpool2_grad(dH1 * (P1 > 0.0), code1)
         dWc1 = conv_weight_grad(dZ1, cols1, Wc1.shape)
         dbc1 = dZ1.sum(axis=(0, 2, 3))
-        G[i] = np.concatenate([dWc1.ravel(), dbc1, dWc2.ravel(), dbc2, dWf1.ravel(), dbf1,
-                               dWf2.ravel(), dbf2])
+        G[i] = np.concatenate([dWf1.ravel(), dbf1, dWf2.ravel(), dbf2,
+                               dWc1.ravel(), dbc1, dWc2.ravel(), dbc2])
         loss[i] = ce.mean()
         if return_preact:
-            A_all[i] = A3
+            dec.append({"Z1": Z1, "Z2": Z2, "A3": A3})
     if return_preact:
-        return G, loss, A_all
+        return G, loss, dec
     return G, loss
 
 

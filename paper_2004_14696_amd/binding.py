@@ -18,7 +18,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libdbw.so")
 
 DBW_OK, DBW_EINVAL, DBW_ERANGE, DBW_EHIP, DBW_ESTATE, DBW_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
-DBW_SOFTMAX, DBW_MLP = 0, 1
+DBW_SOFTMAX, DBW_MLP, DBW_CNN = 0, 1, 2
 DBW_CLOCK_FRESH, DBW_CLOCK_PSW, DBW_CLOCK_PSI = 0, 1, 2
 DBW_POLICY_DBW, DBW_POLICY_STATIC, DBW_POLICY_BLIND = 0, 1, 2
 DBW_ESTIMATOR_ISOTONIC, DBW_ESTIMATOR_NAIVE = 0, 1
@@ -147,7 +147,7 @@ def make_config(model: str | int, n: int, B: int, d: int, C: int, H: int = 0, et
                 policy: str | int = DBW_POLICY_DBW, k_static: int = 0,
                 estimator: str | int = DBW_ESTIMATOR_ISOTONIC, g_rows: str | int = DBW_G_ROWS_ALL) -> Config:
     if isinstance(model, str):
-        model = {"softmax": DBW_SOFTMAX, "mlp": DBW_MLP}[model]
+        model = {"softmax": DBW_SOFTMAX, "mlp": DBW_MLP, "cnn": DBW_CNN}[model]
     if isinstance(clock, str):
         clock = CLOCKS[clock]
     if isinstance(policy, str):

@@ -85,6 +85,16 @@ struct dbw_ctx {
   double* part = nullptr;
   float* Hh = nullptr;
   float* dA = nullptr;
+  // CNN workspace
+  float* cH1 = nullptr;
+  uint8_t* cCode1 = nullptr;
+  float* cF = nullptr;
+  uint8_t* cCode2 = nullptr;
+  int32_t* cYlab = nullptr;
+  float* cdP2 = nullptr;
+  float* cdP1 = nullptr;
+  float* cPart1 = nullptr;
+  float* cPart2 = nullptr;
 
   // pinned host staging (coherent; kernels read and write it in place)
   double* h_T = nullptr;        // [kSlots][n]
@@ -171,11 +181,14 @@ bool config_ok(const dbw_config* c, std::string* why) {
     *why = "config is NULL";
     return false;
   }
-  if (c->model != DBW_SOFTMAX && c->model != DBW_MLP) *why = "model must be DBW_SOFTMAX or DBW_MLP";
+  if (c->model != DBW_SOFTMAX && c->model != DBW_MLP && c->model != DBW_CNN)
+    *why = "model must be DBW_SOFTMAX, DBW_MLP or DBW_CNN";
   else if (c->n < 1 || c->n > DBW_MAX_N) *why = "n outside [1, DBW_MAX_N]";
   else if (c->B < 1 || c->d < 1) *why = "B and d must be >= 1";
   else if (c->C < 2 || c->C > 4096) *why = "C outside [2, 4096]";
   else if (c->model == DBW_MLP && (c->H < 1 || c->H > 65536)) *why = "H outside [1, 65536]";
+  else if (c->model == DBW_CNN && c->d != dbw::CNN_IMG * dbw::CNN_IMG) *why = "the CNN takes d = 784 (28 x 28 images)";
+  else if (c->model == DBW_CNN && (c->H < 1 || c->H > 65536)) *why = "H outside [1, 65536]";
   else if (c->D < 1 || c->D > DBW_MAX_D) *why = "D outside [1, DBW_MAX_D]";
   else if (!(c->eta > 0.0) || !std::isfinite(c->eta)) *why = "eta must be finite and > 0";
   else if (!(c->beta >= 1.0) || !std::isfinite(c->beta)) *why = "beta must be finite and >= 1";
@@ -197,6 +210,8 @@ bool config_ok(const dbw_config* c, std::string* why) {
 
 int64_t param_count(const dbw_config& c) {
   if (c.model == DBW_SOFTMAX) return (int64_t)c.d * c.C;
+  if (c.model == DBW_CNN)
+    return (int64_t)dbw::CNN_FEAT * c.H + c.H + (int64_t)c.H * c.C + c.C + dbw::CNN_CONV_PARAMS;
   return (int64_t)c.d * c.H + c.H + (int64_t)c.H * c.C + c.C;
 }
 
@@ -445,6 +460,16 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.err = c->err;
     a.keep_slabs = keep_slabs ? 1 : 0;
     e = dbw::launch_softmax_grads(c->splan, a, c->stream);
+  } else if (cf.model == DBW_CNN) {
+    dbw::CnnArgs a{};
+    a.w = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
+    a.n = cf.n; a.B = cf.B; a.H = cf.H; a.C = cf.C;
+    a.P = c->P; a.off_c1 = c->P - dbw::CNN_CONV_PARAMS; a.off_c2 = a.off_c1 + dbw::CNN_C1 * 25 + dbw::CNN_C1;
+    a.G = G; a.loss = loss;
+    a.H1 = c->cH1; a.code1 = c->cCode1; a.F = c->cF; a.code2 = c->cCode2; a.ylab = c->cYlab;
+    a.dP2 = c->cdP2; a.dP1 = c->cdP1; a.part1 = c->cPart1; a.part2 = c->cPart2; a.chunk = dbw::kCnnChunk;
+    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err;
+    e = dbw::launch_cnn_grads(c->mplan, a, c->stream);
   } else {
     dbw::MlpArgs a{};
     a.w = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
@@ -489,7 +514,8 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
     const int64_t lim = dbw::kMaxBufferBytes;
     if (P * 4 > lim || (int64_t)cfg->n * cfg->B * cfg->d * 4 > lim || cfg->S * cfg->d * 4 > lim ||
         (int64_t)cfg->n * cfg->B * cfg->C * 4 > lim ||
-        (cfg->model == DBW_MLP && (int64_t)cfg->n * cfg->B * cfg->H * 4 > lim))
+        (cfg->model != DBW_SOFTMAX && (int64_t)cfg->n * cfg->B * cfg->H * 4 > lim) ||
+        (cfg->model == DBW_CNN && (int64_t)cfg->n * cfg->B * dbw::CNN_C1 * 144 * 4 > lim))
       return DBW_EUNSUPPORTED;
   }
   dbw_ctx* c = new (std::nothrow) dbw_ctx();
@@ -506,7 +532,8 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   if (cf.model == DBW_SOFTMAX) {
     c->splan = dbw::softmax_plan(cf.n, cf.B, cf.d, cf.C);
   } else {
-    c->mplan = dbw::mlp_plan(cf.n, cf.B, cf.d, cf.H, cf.C);
+    // the CNN's fully connected part is the MLP on its 800 features
+    c->mplan = dbw::mlp_plan(cf.n, cf.B, cf.model == DBW_CNN ? dbw::CNN_FEAT : cf.d, cf.H, cf.C);
     if (!c->mplan.ok) {
       delete c;
       return DBW_EUNSUPPORTED;
@@ -536,7 +563,7 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
        sSel = take(sizeof(int32_t) * n), sTicks = take(sizeof(int64_t) * n),
        sSt = take(sizeof(dbw_estimator_state)), sErr = take(4),
        sSqp = take(sizeof(float) * n * part_blocks), sPart = take(sizeof(double) * 2 * part_blocks);
-  Span sGp, sLp, sZ, sCe, sH, sdA;
+  Span sGp, sLp, sZ, sCe, sH, sdA, sH1, sC1, sF, sC2, sYl, sdP2, sdP1, sPa1, sPa2;
   if (cf.model == DBW_SOFTMAX) {
     if (c->splan.fused) {
       if (c->splan.slabs > 1) {
@@ -552,6 +579,18 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
     sdA = take(sizeof(float) * rowsN * cf.H);
     sGp = take(sizeof(float) * n * c->mplan.slabs * c->mplan.tail);
     sLp = take(sizeof(float) * n * c->mplan.slabs);
+    if (cf.model == DBW_CNN) {
+      const int64_t h1 = rowsN * dbw::CNN_C1 * 144, ch = dbw::cnn_chunks(cf.B);
+      sH1 = take(sizeof(float) * h1);
+      sC1 = take(h1);
+      sF = take(sizeof(float) * rowsN * dbw::CNN_FEAT);
+      sC2 = take(rowsN * dbw::CNN_FEAT);
+      sYl = take(sizeof(int32_t) * rowsN);
+      sdP2 = take(sizeof(float) * rowsN * dbw::CNN_FEAT);
+      sdP1 = take(sizeof(float) * h1);
+      sPa1 = take(sizeof(float) * n * ch * (dbw::CNN_C1 * 25 + dbw::CNN_C1));
+      sPa2 = take(sizeof(float) * n * ch * (dbw::CNN_C2 * dbw::CNN_C1 * 25 + dbw::CNN_C2));
+    }
   }
   if (hipMalloc(&c->pool, total) != hipSuccess) {
     delete c;
@@ -565,6 +604,9 @@ DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out
   c->err = (int32_t*)at(sErr); c->sqpart = (float*)at(sSqp); c->part = (double*)at(sPart);
   c->Gp = (float*)at(sGp); c->lossp = (float*)at(sLp);
   c->Z = (float*)at(sZ); c->ce = (float*)at(sCe); c->Hh = (float*)at(sH); c->dA = (float*)at(sdA);
+  c->cH1 = (float*)at(sH1); c->cCode1 = (uint8_t*)at(sC1); c->cF = (float*)at(sF); c->cCode2 = (uint8_t*)at(sC2);
+  c->cYlab = (int32_t*)at(sYl); c->cdP2 = (float*)at(sdP2); c->cdP1 = (float*)at(sdP1);
+  c->cPart1 = (float*)at(sPa1); c->cPart2 = (float*)at(sPa2);
 
   bool ok = hipMemset(c->pool, 0, total) == hipSuccess;
   const unsigned pin = hipHostMallocMapped | hipHostMallocCoherent;

@@ -77,7 +77,8 @@ struct MlpArgs {
   const int32_t* rows;
   int64_t S;
   int n, B, d, H, C;
-  float* G;              // [n][P]
+  float* G;              // [n][ldG]: the MLP's P floats at the start of each row
+  int64_t ldG;           // row stride of G (0: P)
   float* loss;           // [n]
   // workspace
   float* Hh;             // [n*B][H] hidden activations
@@ -88,6 +89,42 @@ struct MlpArgs {
 };
 MlpPlan mlp_plan(int n, int B, int d, int H, int C);
 hipError_t launch_mlp_grads(const MlpPlan& plan, const MlpArgs& a, hipStream_t s);
+
+// The MNIST-shaped CNN: 28 x 28 images, conv 5 x 5 to 20 channels, 2 x 2 max
+// pooling, ReLU, conv 5 x 5 to 50 channels, pooling, ReLU, then the MLP
+// 800-H-C.  Parameters [MLP (800-H-C) | Wc1 (20x1x5x5) | bc1 | Wc2 (50x20x5x5) | bc2].
+constexpr int CNN_IMG = 28, CNN_C1 = 20, CNN_C2 = 50, CNN_FEAT = 800;
+constexpr int64_t CNN_CONV_PARAMS = CNN_C1 * 25 + CNN_C1 + CNN_C2 * CNN_C1 * 25 + CNN_C2;
+constexpr int kCnnChunk = 16;   // images per weight-gradient partial
+struct CnnArgs {
+  const float* w;        // [P]
+  const float* X;        // [n*B][784] or dataset [S][784]
+  const int32_t* y;
+  const int32_t* rows;   // nullable [n*B]
+  int64_t S;
+  int n, B, H, C;
+  int64_t P, off_c1, off_c2;   // parameter count, offsets of Wc1 and Wc2
+  float* G;              // [n][P]
+  float* loss;           // [n]
+  // workspace
+  float* H1;             // [n*B][20][12][12] pooled, ReLU'd conv1 output
+  uint8_t* code1;        // [n*B][20][12][12] window code of each pooled value
+  float* F;              // [n*B][800] pooled, ReLU'd conv2 output (the features)
+  uint8_t* code2;        // [n*B][800]
+  int32_t* ylab;         // [n*B] gathered labels
+  float* dP2;            // [n*B][800] gradient at the features, ReLU-masked
+  float* dP1;            // [n*B][2880] gradient at H1, ReLU-masked
+  float* part1;          // [n][chunks][520] conv1 weight-gradient partials
+  float* part2;          // [n][chunks][25050] conv2 weight-gradient partials
+  int chunk;             // images per partial
+  float* Hh;             // MLP workspace
+  float* dA;
+  float* Gp;
+  float* lossp;
+  int32_t* err;
+};
+int cnn_chunks(int B);
+hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // PS side.

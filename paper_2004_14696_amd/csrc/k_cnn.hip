@@ -1,0 +1,432 @@
+// Worker minibatch gradients of the MNIST-shaped CNN (Sect. 4: two 5x5
+// convolutions and two fully connected layers; Sect. 2, Eq. gradient), gfx950.
+//
+// Per image (28 x 28, one channel): conv 1 -> 20 channels (24 x 24), 2 x 2 max
+// pooling and ReLU (20 x 12 x 12 = H1), conv 20 -> 50 (8 x 8), pooling and ReLU
+// (50 x 4 x 4 = the 800 features F), then the fully connected part, which is
+// the MLP 800-H-C (k_mlp.hip).  A pooling window passes its first largest
+// value in row-major order; only that entry receives the gradient.
+//
+//  k_cnn_conv1_pool   one thread per pooled position of an image: the four
+//                     conv outputs of its window for all 20 filters (vector
+//                     ALU, filters in LDS), the pooled value, its ReLU and the
+//                     window code; also gathers the image's label.
+//  k_cnn_conv2_pool   one block per image: the conv as a 64 x 64 x 500 GEMM on
+//                     the fp32 matrix cores (positions x filters x (channel,
+//                     row, column) of the 5 x 5 patches), the image's H1 staged
+//                     in LDS; pooling and ReLU in the epilogue.
+//  k_cnn_dfeat        dF = dA Wf1^T (matrix cores) masked by the ReLU of F: the
+//                     gradient at the pooled conv2 outputs.
+//  k_cnn_conv2_dgrad  gradient at H1: every nonzero pooled gradient g of filter
+//                     o, placed at its window's passing entry (y, x), adds
+//                     g W2[o][c][u][v] to H1 position (c, y+u, x+v).  A wave owns
+//                     two input channels c and all their 25 (u, v): its lanes
+//                     hit distinct positions, and no other wave touches them, so
+//                     the LDS accumulation needs no atomics and runs in a fixed
+//                     order.  Then the ReLU mask of H1.
+//  k_cnn_conv2_wgrad  dW2 and db2 partials over chunks of a worker's images:
+//                     lane (c, u, v) accumulates for the 50 filters the H1
+//                     value under each nonzero pooled gradient.
+//  k_cnn_conv1_wgrad  dW1 and db1 partials: lane (o, u, v) accumulates over the
+//                     144 pooled positions of each image of the chunk.
+//  k_cnn_wreduce      sums the chunk partials in chunk order into G.
+//
+// Everything runs in a fixed order: results are bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "dbw_buffer.h"
+#include "dbw_internal.h"
+#include "mfma_gemm.h"
+
+namespace dbw {
+namespace {
+
+constexpr int IMG = CNN_IMG, KS = 5, NC1 = CNN_C1, NC2 = CNN_C2;
+constexpr int Q1 = 12, NPOS1 = Q1 * Q1, H1LEN = NC1 * NPOS1;   // 2880 per image
+constexpr int O2 = 8, NPOS2 = O2 * O2;                          // conv2 output positions
+constexpr int Q2 = 4, NQ2 = Q2 * Q2, FEAT = CNN_FEAT;           // 800
+constexpr int K2 = NC1 * KS * KS;                               // 500: conv2 patch length
+constexpr int W1LEN = NC1 * KS * KS;                            // 500 conv1 weights
+
+__device__ __forceinline__ int64_t cnn_row(const CnnArgs& a, int64_t m, bool report) {
+  if (!a.rows) return m;
+  const int64_t r = a.rows[m];
+  if (r < 0 || r >= a.S) {
+    if (report) atomicOr(a.err, ERR_ROW_RANGE);
+    return -1;
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_cnn_conv1_pool(CnnArgs a) {
+  __shared__ float sw[W1LEN + NC1];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < W1LEN + NC1; i += 256) sw[i] = a.w[a.off_c1 + i];   // W1 then b1
+  __syncthreads();
+  const int64_t nB = (int64_t)a.n * a.B;
+  const int64_t gidx = (int64_t)blockIdx.x * 256 + tid;
+  if (gidx >= nB * NPOS1) return;
+  const int64_t b = gidx / NPOS1;
+  const int pos = static_cast<int>(gidx - b * NPOS1), py = pos / Q1, px = pos % Q1;
+  const int64_t row = cnn_row(a, b, pos == 0);
+  if (pos == 0) {
+    int lab = row >= 0 ? a.y[row] : 0;
+    if (lab < 0 || lab >= a.C) {
+      atomicOr(a.err, ERR_LABEL_RANGE);
+      lab = 0;
+    }
+    a.ylab[b] = lab;
+  }
+  // the 6 x 6 input patch under the window's four 5 x 5 filters
+  float in[6][6];
+  const float* img = a.X + (row >= 0 ? row : 0) * (int64_t)(IMG * IMG);
+#pragma unroll
+  for (int r = 0; r < 6; ++r)
+#pragma unroll
+    for (int c = 0; c < 6; ++c) in[r][c] = row >= 0 ? img[(2 * py + r) * IMG + 2 * px + c] : 0.f;
+  float* h1 = a.H1 + b * H1LEN + pos;
+  uint8_t* cd = a.code1 + b * H1LEN + pos;
+#pragma unroll 1
+  for (int o = 0; o < NC1; ++o) {
+    float z[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int dy = q >> 1, dx = q & 1;
+      float s = sw[W1LEN + o];
+#pragma unroll
+      for (int u = 0; u < KS; ++u)
+#pragma unroll
+        for (int v = 0; v < KS; ++v) s = fmaf(in[dy + u][dx + v], sw[o * 25 + u * KS + v], s);
+      z[q] = s;
+    }
+    int code = 0;
+    float best = z[0];
+#pragma unroll
+    for (int q = 1; q < 4; ++q)
+      if (z[q] > best) {
+        best = z[q];
+        code = q;
+      }
+    h1[o * NPOS1] = best > 0.f ? best : 0.f;
+    cd[o * NPOS1] = static_cast<uint8_t>(code);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Conv2 of one image as a GEMM: Z[m][o] = sum_k A[m][k] W2[o][k], m = output
+// position (y, x) of the 8 x 8, k = (c, u, v), A[m][k] = H1[c][y+u][x+v].
+struct Conv2Lds {
+  MfmaLds<2> g;
+  float h1[H1LEN];
+  float z[NPOS2][NC2 + 1];
+};
+
+__global__ __launch_bounds__(256) void k_cnn_conv2_pool(CnnArgs a) {
+  __shared__ Conv2Lds L;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int64_t b = blockIdx.x;
+  for (int i = tid; i < H1LEN; i += 256) L.h1[i] = a.H1[b * H1LEN + i];
+  const float* W2 = a.w + a.off_c2;
+  // slice loads: A [16 k][64 m] from LDS, B [16 k][64 o] from W2 (L2)
+  auto load = [&](int k0, float (&ra)[4], float (&rb)[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      const int ka = k0 + e / 64, m = e % 64;
+      const int c = ka / 25, uv = ka % 25;
+      const int y = m >> 3, x = m & 7;
+      ra[s] = ka < K2 ? L.h1[c * NPOS1 + (y + uv / 5) * Q1 + x + uv % 5] : 0.f;
+      const int kb = k0 + e % 16, o = e / 16;
+      rb[s] = kb < K2 && o < NC2 ? W2[o * K2 + kb] : 0.f;
+    }
+  };
+  auto store = [&](int buf, const float (&ra)[4], const float (&rb)[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      L.g.A[buf][e / 64][e % 64] = ra[s];
+      L.g.B[buf][e % 16][e / 16] = rb[s];
+    }
+  };
+  __syncthreads();
+  mfma_f32x4 acc[2][2];
+  mfma_zero<2>(acc);
+  float ra[4], rb[4];
+  load(0, ra, rb);
+  store(0, ra, rb);
+  __syncthreads();
+  constexpr int NK = (K2 + MBK - 1) / MBK;
+  for (int kt = 0; kt < NK; ++kt) {
+    const int cbuf = kt & 1;
+    if (kt + 1 < NK) load((kt + 1) * MBK, ra, rb);
+    mfma_slice<2>(L.g, cbuf, wm, wn, lane, acc);
+    if (kt + 1 < NK) store(cbuf ^ 1, ra, rb);
+    __syncthreads();
+  }
+  // bias, then the 2 x 2 pooling of every filter's 8 x 8 map
+  const float* b2 = a.w + a.off_c2 + NC2 * K2;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = wm * 32 + mt * 16 + 4 * (lane >> 4) + r;
+        const int o = wn * 32 + nt * 16 + (lane & 15);
+        if (o < NC2) L.z[m][o] = acc[mt][nt][r] + b2[o];
+      }
+  __syncthreads();
+  for (int f = tid; f < FEAT; f += 256) {
+    const int o = f / NQ2, q = f % NQ2, y = 2 * (q / Q2), x = 2 * (q % Q2);
+    float best = L.z[y * O2 + x][o];
+    int code = 0;
+    const float z1 = L.z[y * O2 + x + 1][o], z2 = L.z[(y + 1) * O2 + x][o], z3 = L.z[(y + 1) * O2 + x + 1][o];
+    if (z1 > best) { best = z1; code = 1; }
+    if (z2 > best) { best = z2; code = 2; }
+    if (z3 > best) { best = z3; code = 3; }
+    a.F[b * FEAT + f] = best > 0.f ? best : 0.f;
+    a.code2[b * FEAT + f] = static_cast<uint8_t>(code);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dP2[m][f] = (sum_h dA[m][h] Wf1[f][h]) [F[m][f] > 0]; 64 x 64 tiles.
+__global__ __launch_bounds__(256) void k_cnn_dfeat(CnnArgs a) {
+  __shared__ MfmaLds<2> L;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int64_t nB = (int64_t)a.n * a.B;
+  const int H = a.H;
+  const int n0 = blockIdx.x * 64;
+  const int64_t m0 = (int64_t)blockIdx.y * 64;
+  const float* Wf1 = a.w;     // [800][H]
+  auto load = [&](int k0, float (&ra)[4], float (&rb)[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      const int k = k0 + e % 16, i = e / 16;
+      const int64_t m = m0 + i;
+      ra[s] = k < H && m < nB ? a.dA[m * H + k] : 0.f;
+      const int f = n0 + i;
+      rb[s] = k < H && f < FEAT ? Wf1[(int64_t)f * H + k] : 0.f;
+    }
+  };
+  auto store = [&](int buf, const float (&ra)[4], const float (&rb)[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      L.A[buf][e % 16][e / 16] = ra[s];
+      L.B[buf][e % 16][e / 16] = rb[s];
+    }
+  };
+  mfma_f32x4 acc[2][2];
+  mfma_zero<2>(acc);
+  float ra[4], rb[4];
+  load(0, ra, rb);
+  store(0, ra, rb);
+  __syncthreads();
+  const int nk = (H + MBK - 1) / MBK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cbuf = kt & 1;
+    if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
+    mfma_slice<2>(L, cbuf, wm, wn, lane, acc);
+    if (kt + 1 < nk) store(cbuf ^ 1, ra, rb);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t m = m0 + wm * 32 + mt * 16 + 4 * (lane >> 4) + r;
+        const int f = n0 + wn * 32 + nt * 16 + (lane & 15);
+        if (m < nB && f < FEAT) a.dP2[m * FEAT + f] = a.F[m * FEAT + f] > 0.f ? acc[mt][nt][r] : 0.f;
+      }
+}
+
+// ---------------------------------------------------------------------------
+// Gradient at H1, one image per loop step (blocks stride over the images).
+constexpr int DG_WAVES = NC1 / 2;   // a wave per two input channels
+__global__ __launch_bounds__(DG_WAVES * 64) void k_cnn_conv2_dgrad(CnnArgs a) {
+  __shared__ float sg[FEAT];
+  __shared__ uint8_t scode[FEAT];
+  __shared__ float sdh[H1LEN];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const bool active = lane < 50;
+  const int c = 2 * wv + (lane >= 25 ? 1 : 0), uv = active ? lane % 25 : 0;
+  const int u = uv / 5, v = uv % 5;
+  // this lane's filter taps W2[o][c][u][v] for the 50 filters
+  float wcol[NC2];
+  const float* W2 = a.w + a.off_c2;
+#pragma unroll
+  for (int o = 0; o < NC2; ++o) wcol[o] = active ? W2[o * K2 + c * 25 + uv] : 0.f;
+  const int64_t nB = (int64_t)a.n * a.B;
+  for (int64_t b = blockIdx.x; b < nB; b += gridDim.x) {
+    for (int i = tid; i < FEAT; i += blockDim.x) {
+      sg[i] = a.dP2[b * FEAT + i];
+      scode[i] = a.code2[b * FEAT + i];
+    }
+    for (int i = tid; i < H1LEN; i += blockDim.x) sdh[i] = 0.f;
+    __syncthreads();
+    if (active) {
+      float* dh = sdh + c * NPOS1 + u * Q1 + v;
+      for (int q = 0; q < NQ2; ++q) {
+        float* dq = dh + 2 * (q / Q2) * Q1 + 2 * (q % Q2);
+#pragma unroll
+        for (int o = 0; o < NC2; ++o) {   // register index o: fully unrolled
+          const float g = sg[o * NQ2 + q];
+          if (g == 0.f) continue;          // the same in every lane
+          const int cd = scode[o * NQ2 + q];
+          float* t = dq + (cd >> 1) * Q1 + (cd & 1);
+          *t = fmaf(g, wcol[o], *t);
+        }
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < H1LEN; i += blockDim.x)
+      a.dP1[b * H1LEN + i] = a.H1[b * H1LEN + i] > 0.f ? sdh[i] : 0.f;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dW2, db2 partial of chunk j of worker i: images i B + j*chunk .. (in order).
+__global__ __launch_bounds__(512) void k_cnn_conv2_wgrad(CnnArgs a) {
+  __shared__ float sh1[H1LEN];
+  __shared__ float sg[FEAT];
+  __shared__ uint8_t scode[FEAT];
+  const int tid = threadIdx.x;
+  const int i = blockIdx.y, j = blockIdx.x;
+  const bool active = tid < K2;
+  const int c = active ? tid / 25 : 0, uv = active ? tid % 25 : 0, u = uv / 5, v = uv % 5;
+  float acc[NC2];
+#pragma unroll
+  for (int o = 0; o < NC2; ++o) acc[o] = 0.f;
+  float db = 0.f;
+  const int b0 = j * a.chunk, b1 = min(a.B, b0 + a.chunk);
+  for (int bb = b0; bb < b1; ++bb) {
+    const int64_t b = (int64_t)i * a.B + bb;
+    for (int e = tid; e < H1LEN; e += blockDim.x) sh1[e] = a.H1[b * H1LEN + e];
+    for (int e = tid; e < FEAT; e += blockDim.x) {
+      sg[e] = a.dP2[b * FEAT + e];
+      scode[e] = a.code2[b * FEAT + e];
+    }
+    __syncthreads();
+    if (active) {
+      const float* h = sh1 + c * NPOS1 + u * Q1 + v;
+      for (int q = 0; q < NQ2; ++q) {
+        const float* hq = h + 2 * (q / Q2) * Q1 + 2 * (q % Q2);
+#pragma unroll
+        for (int o = 0; o < NC2; ++o) {   // register index o: fully unrolled
+          const float g = sg[o * NQ2 + q];
+          if (g == 0.f) continue;          // the same in every lane
+          const int cd = scode[o * NQ2 + q];
+          acc[o] = fmaf(g, hq[(cd >> 1) * Q1 + (cd & 1)], acc[o]);
+        }
+      }
+    }
+    if (tid < NC2) {
+      float s = 0.f;
+      for (int q = 0; q < NQ2; ++q) s += sg[tid * NQ2 + q];
+      db += s;
+    }
+    __syncthreads();
+  }
+  // partial [i][j][W2 (50 x 500) | b2 (50)]
+  float* p = a.part2 + ((int64_t)i * gridDim.x + j) * (NC2 * K2 + NC2);
+  if (active)
+#pragma unroll
+    for (int o = 0; o < NC2; ++o) p[o * K2 + tid] = acc[o];
+  if (tid < NC2) p[NC2 * K2 + tid] = db;
+}
+
+// ---------------------------------------------------------------------------
+// dW1, db1 partial of chunk j of worker i.
+__global__ __launch_bounds__(512) void k_cnn_conv1_wgrad(CnnArgs a) {
+  __shared__ float sx[IMG * IMG];
+  __shared__ float sg[H1LEN];
+  __shared__ uint8_t scode[H1LEN];
+  const int tid = threadIdx.x;
+  const int i = blockIdx.y, j = blockIdx.x;
+  const bool active = tid < W1LEN;
+  const int o = active ? tid / 25 : 0, uv = active ? tid % 25 : 0, u = uv / 5, v = uv % 5;
+  float acc = 0.f, db = 0.f;
+  const int b0 = j * a.chunk, b1 = min(a.B, b0 + a.chunk);
+  for (int bb = b0; bb < b1; ++bb) {
+    const int64_t b = (int64_t)i * a.B + bb;
+    const int64_t row = cnn_row(a, b, false);
+    for (int e = tid; e < IMG * IMG; e += blockDim.x) sx[e] = row >= 0 ? a.X[row * (IMG * IMG) + e] : 0.f;
+    for (int e = tid; e < H1LEN; e += blockDim.x) {
+      sg[e] = a.dP1[b * H1LEN + e];
+      scode[e] = a.code1[b * H1LEN + e];
+    }
+    __syncthreads();
+    if (active) {
+      const float* g = sg + o * NPOS1;
+      const uint8_t* cd = scode + o * NPOS1;
+      const float* xs = sx + u * IMG + v;
+      for (int p = 0; p < NPOS1; ++p) {
+        const int y = 2 * (p / Q1) + (cd[p] >> 1), x = 2 * (p % Q1) + (cd[p] & 1);
+        acc = fmaf(g[p], xs[y * IMG + x], acc);
+        if (uv == 0) db += g[p];
+      }
+    }
+    __syncthreads();
+  }
+  // partial [i][j][W1 (20 x 25) | b1 (20)]
+  float* p = a.part1 + ((int64_t)i * gridDim.x + j) * (W1LEN + NC1);
+  if (active) p[tid] = acc;
+  if (active && uv == 0) p[W1LEN + o] = db;
+}
+
+// ---------------------------------------------------------------------------
+// G[i][off_c1 + e] = sum over chunks in order of the partials (conv1 block
+// then conv2 block, which are contiguous in w).
+__global__ __launch_bounds__(256) void k_cnn_wreduce(CnnArgs a, int chunks) {
+  const int i = blockIdx.y;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  constexpr int L1 = W1LEN + NC1, L2 = NC2 * K2 + NC2;
+  if (e >= L1 + L2) return;
+  float s = 0.f;
+  if (e < L1) {
+    for (int j = 0; j < chunks; ++j) s += a.part1[((int64_t)i * chunks + j) * L1 + e];
+  } else {
+    for (int j = 0; j < chunks; ++j) s += a.part2[((int64_t)i * chunks + j) * L2 + (e - L1)];
+  }
+  a.G[(int64_t)i * a.P + a.off_c1 + e] = s;
+}
+
+}  // namespace
+
+int cnn_chunks(int B) { return (B + kCnnChunk - 1) / kCnnChunk; }
+
+hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t s) {
+  const int64_t nB = (int64_t)a.n * a.B;
+  hipLaunchKernelGGL(k_cnn_conv1_pool, dim3(static_cast<unsigned>((nB * NPOS1 + 255) / 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_cnn_conv2_pool, dim3(static_cast<unsigned>(nB)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // the fully connected part: the MLP 800-H-C on the features, its G block
+  // at the start of each row of G
+  MlpArgs m{};
+  m.w = a.w; m.X = a.F; m.y = a.ylab; m.rows = nullptr; m.S = 0;
+  m.n = a.n; m.B = a.B; m.d = FEAT; m.H = a.H; m.C = a.C;
+  m.G = a.G; m.ldG = a.P; m.loss = a.loss;
+  m.Hh = a.Hh; m.dA = a.dA; m.Gp = a.Gp; m.lossp = a.lossp; m.err = a.err;
+  e = launch_mlp_grads(mplan, m, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_cnn_dfeat, dim3((FEAT + 63) / 64, static_cast<unsigned>((nB + 63) / 64)), dim3(256), 0, s, a);
+  const int64_t dg_blocks = nB < 1024 ? nB : 1024;
+  hipLaunchKernelGGL(k_cnn_conv2_dgrad, dim3(static_cast<unsigned>(dg_blocks)), dim3(DG_WAVES * 64), 0, s, a);
+  const int chunks = cnn_chunks(a.B);
+  hipLaunchKernelGGL(k_cnn_conv2_wgrad, dim3(chunks, a.n), dim3(512), 0, s, a);
+  hipLaunchKernelGGL(k_cnn_conv1_wgrad, dim3(chunks, a.n), dim3(512), 0, s, a);
+  constexpr int LW = W1LEN + NC1 + NC2 * K2 + NC2;
+  hipLaunchKernelGGL(k_cnn_wreduce, dim3((LW + 255) / 256, a.n), dim3(256), 0, s, a, chunks);
+  return hipGetLastError();
+}
+
+}  // namespace dbw

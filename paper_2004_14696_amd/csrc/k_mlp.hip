@@ -178,7 +178,7 @@ __global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a) {
   const int i = blockIdx.z;
   const int j0 = blockIdx.y * BM, n0 = blockIdx.x * BM;
   const int d = a.d, H = a.H, B = a.B;
-  const int64_t P = (int64_t)d * H + H + (int64_t)H * a.C + a.C;
+  const int64_t P = a.ldG ? a.ldG : (int64_t)d * H + H + (int64_t)H * a.C + a.C;   // row stride of G
   const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
   const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
   const __amdgpu_buffer_rsrc_t das = make_rsrc(a.dA + (int64_t)i * B * H, static_cast<uint32_t>((int64_t)B * H * 4));
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a) {
   const int j0 = blockIdx.y * TM;
   const int n0 = blockIdx.x * TN;
   const int d = a.d, H = a.H, B = a.B;
-  const int64_t P = (int64_t)d * H + H + (int64_t)H * a.C + a.C;
+  const int64_t P = a.ldG ? a.ldG : (int64_t)d * H + H + (int64_t)H * a.C + a.C;   // row stride of G
   const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
   const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
   const __amdgpu_buffer_rsrc_t das = make_rsrc(a.dA + (int64_t)i * B * H, static_cast<uint32_t>((int64_t)B * H * 4));
@@ -400,7 +400,7 @@ __global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a) {
 // G[i][d*H + e] = sum_q Gp[i][q][e] for e < L (fixed slab order); loss.
 __global__ __launch_bounds__(256) void k_mlp_tail(MlpArgs a, int slabs, int64_t L) {
   const int i = blockIdx.y;
-  const int64_t P = (int64_t)a.d * a.H + L;
+  const int64_t P = a.ldG ? a.ldG : (int64_t)a.d * a.H + L;   // row stride of G
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e < L) {
     const float* src = a.Gp + (int64_t)i * slabs * L + e;

@@ -11,7 +11,7 @@ from oracle import dbw as odbw
 from oracle import model as omodel
 from oracle import ps as ops
 
-from gpu_util import (RTOL, host, k_acceptable, masked_rel_err, mlp_compare_mask, mlp_inputs, rel_err,
+from gpu_util import (RTOL, cnn_compare_mask, host, k_acceptable, masked_rel_err, mlp_compare_mask, mlp_inputs, rel_err,
                       scalar_rel, softmax_inputs, to_dev)
 
 torch = pytest.importorskip("torch")
@@ -162,6 +162,77 @@ def test_worker_grads_mlp_gathered_and_unsupported_width():
     with pytest.raises(pb.DBWError) as e:           # 3 hidden units per head thread: no kernel
         _ctx(2, 4, 8, 10, model="mlp", H=1100)
     assert e.value.status == pb.DBW_EUNSUPPORTED
+
+
+# -- the CNN -----------------------------------------------------------------------------
+
+def _cnn_inputs(rng, n, B, H, C):
+    """MNIST-like images (most pixels 0) and PyTorch-default initial weights."""
+    X = np.where(rng.random((n, B, 784)) < 0.8, 0.0, rng.random((n, B, 784))).astype(np.float32)
+    y = rng.integers(0, C, size=(n, B), dtype=np.int32)
+    parts = []
+    for shape, fan_in in (((800, H), 800), ((H,), 800), ((H, C), H), ((C,), H),
+                          ((20, 1, 5, 5), 25), ((20,), 25), ((50, 20, 5, 5), 500), ((50,), 500)):
+        b = 1.0 / np.sqrt(fan_in)
+        parts.append(rng.uniform(-b, b, size=shape).astype(np.float32).ravel())
+    return X, y, np.concatenate(parts)
+
+
+@pytest.mark.parametrize("n,B,H,C", [(3, 8, 24, 10), (2, 37, 500, 10), (5, 4, 7, 3)])
+def test_worker_grads_cnn(n, B, H, C):
+    # ragged batches (37 rows: chunks of 16 images plus a tail), a narrow and
+    # the workload's fully connected width
+    rng = np.random.default_rng(3000 + n + B + H)
+    X, y, w = _cnn_inputs(rng, n, B, H, C)
+    ctx = _ctx(n, B, 784, C, model="cnn", H=H)
+    assert ctx.P == w.size == omodel.cnn_param_count(H, C)
+    G, loss = ctx.worker_grads(to_dev(torch, w), to_dev(torch, X), to_dev(torch, y))
+    ctx.sync()
+    Go, lo, dec = omodel.cnn_worker_grads(w.astype(np.float64), X, y, H, C, return_preact=True)
+    masks, amb, conv_out = cnn_compare_mask(dec, H, C)
+    assert conv_out <= n // 2, (amb, conv_out)       # decisions within rounding are rare
+    Gg = host(G)
+    for i in range(n):
+        assert masked_rel_err(Gg[i], Go[i], masks[i]) <= RTOL, i
+    assert rel_err(host(loss), lo) <= RTOL
+
+
+def test_worker_grads_cnn_workload_shape_sampled_workers():
+    # 16 workers x 500 images (the paper's MNIST setting), gathered from a
+    # resident dataset; the oracle checks three of the workers
+    n, B, H, C, S = 16, 500, 500, 10, 3000
+    rng = np.random.default_rng(3100)
+    Xs, _, w = _cnn_inputs(rng, 1, S, H, C)
+    Xs = Xs[0]
+    ys = rng.integers(0, C, size=S, dtype=np.int32)
+    idx = rng.integers(0, S, size=(n, B), dtype=np.int32)
+    ctx = _ctx(n, B, 784, C, model="cnn", H=H, S=S)
+    G, loss = ctx.worker_grads(to_dev(torch, w), to_dev(torch, Xs), to_dev(torch, ys), rows=to_dev(torch, idx))
+    ctx.sync()
+    Gg, lg = host(G), host(loss)
+    for i in (0, 7, 15):
+        Go, lo, dec = omodel.cnn_worker_grads(w.astype(np.float64), Xs[idx[i]][None], ys[idx[i]][None], H, C,
+                                              return_preact=True)
+        masks, amb, conv_out = cnn_compare_mask(dec, H, C)
+        assert masked_rel_err(Gg[i], Go[0], masks[0]) <= RTOL, (i, amb, conv_out)
+        assert lg[i] == pytest.approx(lo[0], rel=RTOL)
+
+
+def test_worker_grads_cnn_rejects_other_image_sizes_and_reports_bad_rows():
+    with pytest.raises(pb.DBWError) as e:
+        _ctx(2, 4, 785, 10, model="cnn", H=16)
+    assert e.value.status == pb.DBW_EINVAL
+    n, B, H, C, S = 2, 4, 16, 10, 50
+    rng = np.random.default_rng(3200)
+    Xs, _, w = _cnn_inputs(rng, 1, S, H, C)
+    ctx = _ctx(n, B, 784, C, model="cnn", H=H, S=S)
+    idx = np.zeros((n, B), np.int32)
+    idx[1, 2] = S                                   # one row past the dataset
+    ctx.worker_grads(to_dev(torch, w), to_dev(torch, Xs[0]), to_dev(torch, np.zeros(S, np.int32)),
+                     rows=to_dev(torch, idx))
+    with pytest.raises(pb.DBWError) as e:
+        ctx.sync()
+    assert e.value.status == pb.DBW_ERANGE
 
 
 # -- aggregation --------------------------------------------------------------------

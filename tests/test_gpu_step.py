@@ -11,12 +11,13 @@ its k sequence is compared with the oracle's up to the first near-tie."""
 import numpy as np
 import pytest
 
-from dbw_inputs import C1, C2, C3, C4, C5, SOFTMAX, DBWConfig, TimeModel, gather, init_params
+from dbw_inputs import C1, C2, C3, C4, C5, C6, SOFTMAX, DBWConfig, TimeModel, gather, init_params
 from dbw_inputs import generate as gen
 from oracle import dbw as odbw
 from oracle import model as omodel
 from oracle import ps as ops
-from gpu_util import RTOL, host, k_acceptable, masked_rel_err, mlp_compare_mask, rel_err, scalar_rel, to_dev
+from gpu_util import (RTOL, cnn_compare_mask, host, k_acceptable, masked_rel_err, mlp_compare_mask, rel_err,
+                      scalar_rel, to_dev)
 
 torch = pytest.importorskip("torch")
 pb = pytest.importorskip("paper_2004_14696_amd")
@@ -137,10 +138,18 @@ def _lockstep(cfg, iters, seed_rows=False):
             _, _, A = omodel.mlp_worker_grads(orc.w, Xt, yt, cfg.H, cfg.C, return_preact=True)
             masks, amb = mlp_compare_mask(A, cfg.d, cfg.H, cfg.C)
             assert amb <= max(16, A.size // 50000), (cfg.name, t, amb)   # rare
+        elif cfg.model == "cnn":
+            _, _, dec = omodel.cnn_worker_grads(orc.w, Xt, yt, cfg.H, cfg.C, return_preact=True)
+            masks, amb, conv_out = cnn_compare_mask(dec, cfg.H, cfg.C)
+            # near-ties are rare per pooling window, not per 500-image batch
+            # (1.4 million windows): there the masked blocks take the GPU's
+            # values below and the rest is compared
+            if cfg.B * 2880 <= 100_000:
+                assert conv_out <= cfg.n // 2, (cfg.name, t, amb, conv_out)
         V_window = odbw.window_mean(orc.hV, cfg.D)
         rec = orc.step(Xt, yt, ticks)
         if masks is not None:
-            # ReLU decisions within rounding of zero may go either way: the
+            # ReLU and pooling decisions within rounding may go either way: the
             # reference takes the GPU's value there and recomputes the mean
             # and the statistics from that with the oracle's functions
             Gh = np.where(masks, rec["G"], host(out["G"]).astype(np.float64))
@@ -222,6 +231,16 @@ def test_lockstep_naive_estimator_push_and_wait_16_workers():
 def test_lockstep_push_interrupt_tiny():
     orc = _lockstep(TINY.replace(clock="psi"), TINY.iters)
     assert len(set(orc.ks)) > 1
+
+
+def test_lockstep_cnn_small():
+    # the MNIST-shaped CNN, 4 workers x 16 images, narrow first FC layer
+    _lockstep(C6.replace(name="C6small", n=4, B=16, H=32, S=800, iters=10), 10)
+
+
+def test_lockstep_cnn_workload_first_iteration():
+    # 16 workers x 500 images, FC 800-500-10 (the oracle takes ~1 min)
+    _lockstep(C6, 1)
 
 
 def test_lockstep_64_workers_first_iterations():
