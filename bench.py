@@ -74,10 +74,20 @@ def grads_bytes(cfg, P: int, gathered: bool) -> int:
 def grads_flops(cfg) -> float:
     """Useful fp32 flops of one worker-gradient launch (no padding): softmax
     logits X W and gradient X^T R; MLP hidden layer, head forward, head
-    backward (dW2 and the hidden-unit residuals) and X^T dA."""
+    backward (dW2 and the hidden-unit residuals) and X^T dA.  CNN per image:
+    both convolutions forward (24x24x20x25 and 8x8x50x500 products), the
+    gradients of the conv2 filters and of its input and of the conv1 filters
+    over the pooled-through positions only (one in four of each 2x2 window
+    carries gradient), and the fully connected part forward and backward
+    (3 x (800 H + H C) products)."""
     M = cfg.n * cfg.B
     if cfg.model == "softmax":
         return 4.0 * M * cfg.d * cfg.C
+    if cfg.model == "cnn":
+        c1 = 24 * 24 * 20 * 25
+        c2 = 8 * 8 * 50 * 500
+        macs = c1 + c2 + 2 * c2 / 4 + c1 / 4 + 3 * (800 * cfg.H + cfg.H * cfg.C)
+        return 2.0 * M * macs
     return 4.0 * M * cfg.d * cfg.H + 6.0 * M * cfg.H * cfg.C
 
 
@@ -273,7 +283,10 @@ def main(argv=None) -> int:
             "workload": f"{cfg.name}: softmax regression, n={cfg.n} workers x B={cfg.B} rows, d={cfg.d}, "
                         f"C={cfg.C}, minibatches gathered by index from a resident {cfg.S}x{cfg.d} dataset"
             if cfg.model == "softmax" else
-            f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows",
+            f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows"
+            if cfg.model == "mlp" else
+            f"{cfg.name}: CNN 28x28 conv5x5(20)-pool-conv5x5(50)-pool-FC{cfg.H}-FC{cfg.C}, "
+            f"n={cfg.n} workers x B={cfg.B} images gathered from a resident {cfg.S}-image dataset",
             "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P, "clock": cfg.clock,
             "policy": cfg.policy, "k_static": cfg.k_static, "estimator": cfg.estimator, "g_rows": cfg.g_rows,
         },
