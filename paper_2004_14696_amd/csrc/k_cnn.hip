@@ -17,16 +17,16 @@
 //                     in LDS; pooling and ReLU in the epilogue.
 //  k_cnn_dfeat        dF = dA Wf1^T (matrix cores) masked by the ReLU of F: the
 //                     gradient at the pooled conv2 outputs.
-//  k_cnn_conv2_dgrad  gradient at H1: every nonzero pooled gradient g of filter
-//                     o, placed at its window's passing entry (y, x), adds
-//                     g W2[o][c][u][v] to H1 position (c, y+u, x+v).  A wave owns
-//                     two input channels c and all their 25 (u, v): its lanes
-//                     hit distinct positions, and no other wave touches them, so
-//                     the LDS accumulation needs no atomics and runs in a fixed
-//                     order.  Then the ReLU mask of H1.
+//  k_cnn_conv2_dgrad  gradient at H1: per image and input channel the GEMM
+//                     dcols = dZ2 W2 (positions x taps, K = filters) on the
+//                     matrix cores, with the filters' fragments held in
+//                     registers by a persistent grid; the fold of dcols back
+//                     onto the 12 x 12 map reads zero-framed tap maps in LDS at
+//                     fixed offsets.  Then the ReLU mask of H1.
 //  k_cnn_conv2_wgrad  dW2 and db2 partials over chunks of a worker's images:
-//                     lane (c, u, v) accumulates for the 50 filters the H1
-//                     value under each nonzero pooled gradient.
+//                     dW2 += dZ2^T im2col(H1) per image (filters x taps, K =
+//                     positions) on the matrix cores, accumulators kept over the
+//                     chunk, the next image staged in LDS meanwhile.
 //  k_cnn_conv1_wgrad  dW1 and db1 partials: lane (o, u, v) accumulates over the
 //                     144 pooled positions of each image of the chunk.
 //  k_cnn_wreduce      sums the chunk partials in chunk order into G.
@@ -248,98 +248,234 @@ __global__ __launch_bounds__(256) void k_cnn_dfeat(CnnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Gradient at H1, one image per loop step (blocks stride over the images).
-constexpr int DG_WAVES = NC1 / 2;   // a wave per two input channels
-__global__ __launch_bounds__(DG_WAVES * 64) void k_cnn_conv2_dgrad(CnnArgs a) {
-  __shared__ float sg[FEAT];
-  __shared__ uint8_t scode[FEAT];
-  __shared__ float sdh[H1LEN];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const bool active = lane < 50;
-  const int c = 2 * wv + (lane >= 25 ? 1 : 0), uv = active ? lane % 25 : 0;
-  const int u = uv / 5, v = uv % 5;
-  // this lane's filter taps W2[o][c][u][v] for the 50 filters
-  float wcol[NC2];
+// Gradient at H1.  Per image the pooled gradient is unpooled into dZ2[m][o]
+// (its value at the window's passing entry, 0 at the other three), and
+// dcols[m][(c, t)] = sum_o dZ2[m][o] W2[o][c][t] is a 64 x 25 x 50 GEMM per
+// input channel c on the matrix cores (4 x 2 tiles of 16 x 16, K = 50 padded
+// to 52).  Each wave owns five channels and holds their W2 fragments in
+// registers for the whole (persistent) launch.  The fold back onto H1,
+// dH1[c][p] = sum_{t = (u, v)} dcols[p - (u, v)][(c, t)], goes through a
+// wave-private LDS copy of the channel's 25 tap maps, each stored in a
+// zero-framed 12 x 12 tile (data in rows and columns 4..11) so that a target's
+// 25 reads sit at fixed offsets from it and out-of-range taps read zeros.
+constexpr int DG_CPW = NC1 / 4;          // channels per wave (4 waves)
+constexpr int DG_KS = (NC2 + 3) / 4;     // 13 K steps of 4 filters
+constexpr int SA_LD = 80;                // unpooled-gradient row stride (bank spread)
+constexpr int DT = 12 * 12;              // one framed tap map
+constexpr int DLEN = 25 * DT + 64;       // 25 maps and a zero tail
+constexpr int kDgradBlocks = 512;        // two blocks per CU
+
+__global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
+  __shared__ float sA[52 * SA_LD];                     // [o][m]
+  __shared__ __align__(16) float sD[4][DLEN];           // per wave
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
+  for (int i = tid; i < 4 * DLEN; i += 256) (&sD[0][0])[i] = 0.f;
+  for (int i = tid; i < 2 * SA_LD; i += 256) sA[NC2 * SA_LD + i] = 0.f;   // rows o = 50, 51
+  // B fragments: W2[o = 4 ks + g][c][t = 16 nt + j] of the wave's channels
   const float* W2 = a.w + a.off_c2;
+  float wb[DG_CPW][2][DG_KS];
 #pragma unroll
-  for (int o = 0; o < NC2; ++o) wcol[o] = active ? W2[o * K2 + c * 25 + uv] : 0.f;
+  for (int ci = 0; ci < DG_CPW; ++ci)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < DG_KS; ++ks) {
+        const int o = 4 * ks + g, t = 16 * nt + j, c = DG_CPW * wv + ci;
+        wb[ci][nt][ks] = o < NC2 && t < 25 ? W2[o * K2 + c * 25 + t] : 0.f;
+      }
+  float* D = sD[wv];
   const int64_t nB = (int64_t)a.n * a.B;
   for (int64_t b = blockIdx.x; b < nB; b += gridDim.x) {
-    for (int i = tid; i < FEAT; i += blockDim.x) {
-      sg[i] = a.dP2[b * FEAT + i];
-      scode[i] = a.code2[b * FEAT + i];
+    // unpool: task (o, q) writes the four entries of its window in row o
+    for (int e = tid; e < FEAT; e += 256) {
+      const int o = e / NQ2, q = e % NQ2;
+      const float gv = a.dP2[b * FEAT + e];
+      const int cd = a.code2[b * FEAT + e];
+      const int m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
+      float* row = sA + o * SA_LD + m0;
+      row[0] = cd == 0 ? gv : 0.f;
+      row[1] = cd == 1 ? gv : 0.f;
+      row[O2] = cd == 2 ? gv : 0.f;
+      row[O2 + 1] = cd == 3 ? gv : 0.f;
     }
-    for (int i = tid; i < H1LEN; i += blockDim.x) sdh[i] = 0.f;
     __syncthreads();
-    if (active) {
-      float* dh = sdh + c * NPOS1 + u * Q1 + v;
-      for (int q = 0; q < NQ2; ++q) {
-        float* dq = dh + 2 * (q / Q2) * Q1 + 2 * (q % Q2);
+#pragma unroll   // register index ci
+    for (int ci = 0; ci < DG_CPW; ++ci) {
+      const int c = DG_CPW * wv + ci;
+      mfma_f32x4 acc[4][2];
 #pragma unroll
-        for (int o = 0; o < NC2; ++o) {   // register index o: fully unrolled
-          const float g = sg[o * NQ2 + q];
-          if (g == 0.f) continue;          // the same in every lane
-          const int cd = scode[o * NQ2 + q];
-          float* t = dq + (cd >> 1) * Q1 + (cd & 1);
-          *t = fmaf(g, wcol[o], *t);
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < DG_KS; ++ks) {
+        float av[4];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) av[mt] = sA[(4 * ks + g) * SA_LD + 16 * mt + j];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], wb[ci][nt][ks], acc[mt][nt], 0, 0, 0);
+      }
+      // acc[mt][nt][r]: m = 16 mt + 4 g + r (y = 2 mt + g / 2, x = 4 (g % 2) + r),
+      // tap t = 16 nt + j
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int t = 16 * nt + j;
+          if (t < 25) {
+            float* cell = D + t * DT + (2 * mt + (g >> 1) + 4) * 12 + 4 * (g & 1) + 4;
+            *reinterpret_cast<float4*>(cell) =
+                make_float4(acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]);
+          }
+        }
+      asm volatile("" ::: "memory");   // the wave's LDS ops stay in program order
+      const float* h1 = a.H1 + b * H1LEN + c * NPOS1;
+      float* dp1 = a.dP1 + b * H1LEN + c * NPOS1;
+#pragma unroll
+      for (int pp = 0; pp < 3; ++pp) {
+        const int p = lane + 64 * pp;
+        if (p < NPOS1) {
+          // framed cell of (t, y = py - u, x = px - v) = p + 52 + 708 u + 143 v
+          const float* src = D + p + 52;
+          float s = 0.f;
+#pragma unroll
+          for (int u = 0; u < KS; ++u)
+#pragma unroll
+            for (int v = 0; v < KS; ++v) s += src[708 * u + 143 * v];
+          dp1[p] = h1[p] > 0.f ? s : 0.f;
         }
       }
+      asm volatile("" ::: "memory");
     }
-    __syncthreads();
-    for (int i = tid; i < H1LEN; i += blockDim.x)
-      a.dP1[b * H1LEN + i] = a.H1[b * H1LEN + i] > 0.f ? sdh[i] : 0.f;
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// dW2, db2 partial of chunk j of worker i: images i B + j*chunk .. (in order).
-__global__ __launch_bounds__(512) void k_cnn_conv2_wgrad(CnnArgs a) {
-  __shared__ float sh1[H1LEN];
-  __shared__ float sg[FEAT];
-  __shared__ uint8_t scode[FEAT];
-  const int tid = threadIdx.x;
-  const int i = blockIdx.y, j = blockIdx.x;
-  const bool active = tid < K2;
-  const int c = active ? tid / 25 : 0, uv = active ? tid % 25 : 0, u = uv / 5, v = uv % 5;
-  float acc[NC2];
+// dW2, db2 partial of chunk j of worker i (images i B + j chunk .., in order):
+// dW2[o][n] += sum_m dZ2[m][o] H1[c][m + t] with n = (c, t) = 25 c + t, a
+// 64 x 512 x 64 GEMM per image on the matrix cores (o padded to 64, n to 512;
+// the padded columns read a zero region).  Each of the four waves owns 8
+// column tiles and keeps its 4 x 8 accumulator tiles over the chunk; the
+// image's H1 and unpooled gradient are staged in LDS, the next image's loads
+// in flight meanwhile.
+constexpr int WG_NT = 8;                 // column tiles per wave
+constexpr int WG_ZERO = H1LEN;           // zero region after the image's H1
+constexpr int WG_H1 = H1LEN + 96;
+struct WgradBuf {
+  float h1[WG_H1];
+  float A[NPOS2 * SA_LD];                // [m][o]
+};
+
+__global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
+  __shared__ __align__(16) WgradBuf L[2];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
+  const int i = blockIdx.y, jc = blockIdx.x;
+  const int b0 = jc * a.chunk, b1 = min(a.B, b0 + a.chunk);
+  for (int e = tid; e < 2 * 96; e += 256) L[e / 96].h1[WG_ZERO + e % 96] = 0.f;
+  for (int e = tid; e < 2 * NPOS2 * (SA_LD - NC2); e += 256) {
+    const int bi = e / (NPOS2 * (SA_LD - NC2)), r = e % (NPOS2 * (SA_LD - NC2));
+    L[bi].A[(r / (SA_LD - NC2)) * SA_LD + NC2 + r % (SA_LD - NC2)] = 0.f;
+  }
+  // per column tile: the lane's H1 offset of tap (c, u, v), or the zero region
+  int colbase[WG_NT];
 #pragma unroll
-  for (int o = 0; o < NC2; ++o) acc[o] = 0.f;
-  float db = 0.f;
-  const int b0 = j * a.chunk, b1 = min(a.B, b0 + a.chunk);
-  for (int bb = b0; bb < b1; ++bb) {
-    const int64_t b = (int64_t)i * a.B + bb;
-    for (int e = tid; e < H1LEN; e += blockDim.x) sh1[e] = a.H1[b * H1LEN + e];
-    for (int e = tid; e < FEAT; e += blockDim.x) {
-      sg[e] = a.dP2[b * FEAT + e];
-      scode[e] = a.code2[b * FEAT + e];
+  for (int nt = 0; nt < WG_NT; ++nt) {
+    const int n = 16 * (WG_NT * wv + nt) + j;
+    const int c = n / 25, t = n % 25;
+    colbase[nt] = (n < K2 ? c * NPOS1 + (t / 5) * Q1 + t % 5 : WG_ZERO) + g;
+  }
+  float4 rh[3];
+  float rg[4];
+  uint8_t rc[4];
+  auto fetch = [&](int64_t b) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int e = tid + 256 * s;
+      rh[s] = e < H1LEN / 4 ? reinterpret_cast<const float4*>(a.H1 + b * H1LEN)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    __syncthreads();
-    if (active) {
-      const float* h = sh1 + c * NPOS1 + u * Q1 + v;
-      for (int q = 0; q < NQ2; ++q) {
-        const float* hq = h + 2 * (q / Q2) * Q1 + 2 * (q % Q2);
 #pragma unroll
-        for (int o = 0; o < NC2; ++o) {   // register index o: fully unrolled
-          const float g = sg[o * NQ2 + q];
-          if (g == 0.f) continue;          // the same in every lane
-          const int cd = scode[o * NQ2 + q];
-          acc[o] = fmaf(g, hq[(cd >> 1) * Q1 + (cd & 1)], acc[o]);
-        }
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      rg[s] = e < FEAT ? a.dP2[b * FEAT + e] : 0.f;
+      rc[s] = e < FEAT ? a.code2[b * FEAT + e] : 0;
+    }
+  };
+  auto stage = [&](WgradBuf& B) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int e = tid + 256 * s;
+      if (e < H1LEN / 4) reinterpret_cast<float4*>(B.h1)[e] = rh[s];
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      if (e < FEAT) {
+        const int o = e / NQ2, q = e % NQ2, m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
+        float* col = B.A + m0 * SA_LD + o;
+        col[0] = rc[s] == 0 ? rg[s] : 0.f;
+        col[SA_LD] = rc[s] == 1 ? rg[s] : 0.f;
+        col[O2 * SA_LD] = rc[s] == 2 ? rg[s] : 0.f;
+        col[(O2 + 1) * SA_LD] = rc[s] == 3 ? rg[s] : 0.f;
       }
     }
+  };
+  mfma_f32x4 acc[4][WG_NT];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < WG_NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+  float db = 0.f;
+  if (b0 < b1) {
+    fetch((int64_t)i * a.B + b0);
+    stage(L[0]);
+  }
+  __syncthreads();
+  for (int bb = b0; bb < b1; ++bb) {
+    const int cur = (bb - b0) & 1;
+    const int64_t b = (int64_t)i * a.B + bb;
+    if (bb + 1 < b1) fetch(b + 1);
     if (tid < NC2) {
       float s = 0.f;
-      for (int q = 0; q < NQ2; ++q) s += sg[tid * NQ2 + q];
+      for (int q = 0; q < NQ2; ++q) s += a.dP2[b * FEAT + tid * NQ2 + q];
       db += s;
     }
+    const float* A = L[cur].A + g * SA_LD + j;
+    const float* H = L[cur].h1;
+#pragma unroll
+    for (int ks = 0; ks < NPOS2 / 4; ++ks) {
+      // K index m = 4 ks + g: y = ks / 2, x = 4 (ks % 2) + g
+      const int moff = (ks >> 1) * Q1 + 4 * (ks & 1);
+      float av[4], bv[WG_NT];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) av[mt] = A[4 * ks * SA_LD + 16 * mt];
+#pragma unroll
+      for (int nt = 0; nt < WG_NT; ++nt) bv[nt] = H[colbase[nt] + moff];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < WG_NT; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+    }
+    if (bb + 1 < b1) stage(L[cur ^ 1]);
     __syncthreads();
   }
-  // partial [i][j][W2 (50 x 500) | b2 (50)]
-  float* p = a.part2 + ((int64_t)i * gridDim.x + j) * (NC2 * K2 + NC2);
-  if (active)
+  // partial [i][jc][W2 (50 x 500) | b2 (50)]; acc[mt][nt][r] is (o = 16 mt + 4 g + r, n)
+  float* p = a.part2 + ((int64_t)i * gridDim.x + jc) * (NC2 * K2 + NC2);
 #pragma unroll
-    for (int o = 0; o < NC2; ++o) p[o * K2 + tid] = acc[o];
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < WG_NT; ++nt) {
+      const int n = 16 * (WG_NT * wv + nt) + j;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = 16 * mt + 4 * g + r;
+        if (o < NC2 && n < K2) p[o * K2 + n] = acc[mt][nt][r];
+      }
+    }
   if (tid < NC2) p[NC2 * K2 + tid] = db;
 }
 
@@ -419,10 +555,10 @@ hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t 
   e = launch_mlp_grads(mplan, m, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_cnn_dfeat, dim3((FEAT + 63) / 64, static_cast<unsigned>((nB + 63) / 64)), dim3(256), 0, s, a);
-  const int64_t dg_blocks = nB < 1024 ? nB : 1024;
-  hipLaunchKernelGGL(k_cnn_conv2_dgrad, dim3(static_cast<unsigned>(dg_blocks)), dim3(DG_WAVES * 64), 0, s, a);
+  const int64_t dg_blocks = nB < kDgradBlocks ? nB : kDgradBlocks;
+  hipLaunchKernelGGL(k_cnn_conv2_dgrad, dim3(static_cast<unsigned>(dg_blocks)), dim3(256), 0, s, a);
   const int chunks = cnn_chunks(a.B);
-  hipLaunchKernelGGL(k_cnn_conv2_wgrad, dim3(chunks, a.n), dim3(512), 0, s, a);
+  hipLaunchKernelGGL(k_cnn_conv2_wgrad, dim3(chunks, a.n), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_cnn_conv1_wgrad, dim3(chunks, a.n), dim3(512), 0, s, a);
   constexpr int LW = W1LEN + NC1 + NC2 * K2 + NC2;
   hipLaunchKernelGGL(k_cnn_wreduce, dim3((LW + 255) / 256, a.n), dim3(256), 0, s, a, chunks);
