@@ -108,12 +108,12 @@ struct CnnArgs {
   float* loss;           // [n]
   // workspace
   float* H1;             // [n*B][20][12][12] pooled, ReLU'd conv1 output
-  uint8_t* code1;        // [n*B][20][12][12] window code of each pooled value
+  uint8_t* code1;        // [n*B][20][12][12] window code of each pooled value (4: ReLU off)
   float* F;              // [n*B][800] pooled, ReLU'd conv2 output (the features)
-  uint8_t* code2;        // [n*B][800]
+  uint8_t* code2;        // [n*B][800] window codes of the features (4: ReLU off)
   int32_t* ylab;         // [n*B] gathered labels
-  float* dP2;            // [n*B][800] gradient at the features, ReLU-masked
-  float* dP1;            // [n*B][2880] gradient at H1, ReLU-masked
+  float* dP2;            // [n*B][800] gradient at the features (before their ReLU)
+  float* dP1;            // [n*B][2880] gradient at H1 (before its ReLU)
   float* part1;          // [n][chunks][520] conv1 weight-gradient partials
   float* part2;          // [n][chunks][25050] conv2 weight-gradient partials
   int chunk;             // images per partial

@@ -5,30 +5,36 @@
 // pooling and ReLU (20 x 12 x 12 = H1), conv 20 -> 50 (8 x 8), pooling and ReLU
 // (50 x 4 x 4 = the 800 features F), then the fully connected part, which is
 // the MLP 800-H-C (k_mlp.hip).  A pooling window passes its first largest
-// value in row-major order; only that entry receives the gradient.
+// value in row-major order; only that entry receives the gradient, and none
+// when the pooled value is not positive (ReLU).  The window code 0..3 names
+// the passing entry; code 4 marks a window whose ReLU is off, so unpooling
+// by code applies the ReLU mask as well.
 //
 //  k_cnn_conv1_pool   one thread per pooled position of an image: the four
 //                     conv outputs of its window for all 20 filters (vector
 //                     ALU, filters in LDS), the pooled value, its ReLU and the
 //                     window code; also gathers the image's label.
-//  k_cnn_conv2_pool   one block per image: the conv as a 64 x 64 x 500 GEMM on
-//                     the fp32 matrix cores (positions x filters x (channel,
-//                     row, column) of the 5 x 5 patches), the image's H1 staged
-//                     in LDS; pooling and ReLU in the epilogue.
-//  k_cnn_dfeat        dF = dA Wf1^T (matrix cores) masked by the ReLU of F: the
-//                     gradient at the pooled conv2 outputs.
+//  k_cnn_conv2_pool   the conv as a 64 x 64 x 500 GEMM per image on the fp32
+//                     matrix cores (positions x filters x (channel, row,
+//                     column) of the 5 x 5 patches), filter fragments held in
+//                     registers by a persistent grid, the image's H1 in LDS;
+//                     pooling and ReLU in the epilogue.
+//  k_cnn_dfeat        dF = dA Wf1^T on the matrix cores (the ReLU mask of F is
+//                     in the window codes).
 //  k_cnn_conv2_dgrad  gradient at H1: per image and input channel the GEMM
 //                     dcols = dZ2 W2 (positions x taps, K = filters) on the
 //                     matrix cores, with the filters' fragments held in
 //                     registers by a persistent grid; the fold of dcols back
 //                     onto the 12 x 12 map reads zero-framed tap maps in LDS at
-//                     fixed offsets.  Then the ReLU mask of H1.
+//                     fixed offsets.
 //  k_cnn_conv2_wgrad  dW2 and db2 partials over chunks of a worker's images:
 //                     dW2 += dZ2^T im2col(H1) per image (filters x taps, K =
 //                     positions) on the matrix cores, accumulators kept over the
 //                     chunk, the next image staged in LDS meanwhile.
-//  k_cnn_conv1_wgrad  dW1 and db1 partials: lane (o, u, v) accumulates over the
-//                     144 pooled positions of each image of the chunk.
+//  k_cnn_conv1_wgrad  dW1 and db1 partials: dW1 += dZ1 im2col(X) per image
+//                     (filters x taps, K = the 576 conv1 positions) on the
+//                     matrix cores, dZ1 formed from the pooled gradient and
+//                     window codes as the operand is read.
 //  k_cnn_wreduce      sums the chunk partials in chunk order into G.
 //
 // Everything runs in a fixed order: results are bitwise reproducible.
@@ -111,89 +117,108 @@ __global__ __launch_bounds__(256) void k_cnn_conv1_pool(CnnArgs a) {
         code = q;
       }
     h1[o * NPOS1] = best > 0.f ? best : 0.f;
-    cd[o * NPOS1] = static_cast<uint8_t>(code);
+    cd[o * NPOS1] = static_cast<uint8_t>(best > 0.f ? code : 4);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Conv2 of one image as a GEMM: Z[m][o] = sum_k A[m][k] W2[o][k], m = output
+// Conv2 as a GEMM per image: Z[m][o] = sum_k A[m][k] W2[o][k], m = output
 // position (y, x) of the 8 x 8, k = (c, u, v), A[m][k] = H1[c][y+u][x+v].
+// The K steps of 4 run over (tap t, channel quad): step 5 t + cq takes
+// channels 4 cq .. 4 cq + 3 at tap t, so that every A read is the lane's own
+// LDS offset plus a constant.  Wave w owns filters 16 w .. 16 w + 15 and holds
+// their 125 W2 fragments in registers for the whole (persistent) launch; the
+// next image's H1 is loaded while the current one is multiplied.  Bias, 2 x 2
+// pooling and ReLU run from an LDS copy of Z.
+constexpr int FW_KS = K2 / 4;            // 125 K steps
+constexpr int kConvBlocks = 512;         // two blocks per CU
 struct Conv2Lds {
-  MfmaLds<2> g;
-  float h1[H1LEN];
-  float z[NPOS2][NC2 + 1];
+  float h1[2][H1LEN];
+  float z[2][NPOS2][NC2 + 1];
 };
 
-__global__ __launch_bounds__(256) void k_cnn_conv2_pool(CnnArgs a) {
-  __shared__ Conv2Lds L;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
-  const int64_t b = blockIdx.x;
-  for (int i = tid; i < H1LEN; i += 256) L.h1[i] = a.H1[b * H1LEN + i];
+__global__ __launch_bounds__(256, 2) void k_cnn_conv2_pool(CnnArgs a) {
+  __shared__ __align__(16) Conv2Lds L;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
   const float* W2 = a.w + a.off_c2;
-  // slice loads: A [16 k][64 m] from LDS, B [16 k][64 o] from W2 (L2)
-  auto load = [&](int k0, float (&ra)[4], float (&rb)[4]) {
+  const float* b2 = W2 + NC2 * K2;
+  const int o_mine = 16 * wv + j;
+  float wb[FW_KS];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+  for (int t = 0; t < 25; ++t)
+#pragma unroll
+    for (int cq = 0; cq < 5; ++cq)
+      wb[5 * t + cq] = o_mine < NC2 ? W2[o_mine * K2 + (4 * cq + g) * 25 + t] : 0.f;
+  const float bias = o_mine < NC2 ? b2[o_mine] : 0.f;
+  // A operand of lane (g, j): channel 4 cq + g, position m = 16 mt + j
+  const int abase = g * NPOS1 + (j >> 3) * Q1 + (j & 7);
+  const int64_t nB = (int64_t)a.n * a.B;
+  float4 rh[3];
+  auto fetch = [&](int64_t b) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
       const int e = tid + 256 * s;
-      const int ka = k0 + e / 64, m = e % 64;
-      const int c = ka / 25, uv = ka % 25;
-      const int y = m >> 3, x = m & 7;
-      ra[s] = ka < K2 ? L.h1[c * NPOS1 + (y + uv / 5) * Q1 + x + uv % 5] : 0.f;
-      const int kb = k0 + e % 16, o = e / 16;
-      rb[s] = kb < K2 && o < NC2 ? W2[o * K2 + kb] : 0.f;
+      rh[s] = e < H1LEN / 4 ? reinterpret_cast<const float4*>(a.H1 + b * H1LEN)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto store = [&](int buf, const float (&ra)[4], const float (&rb)[4]) {
+  auto stage = [&](float* h) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < 3; ++s) {
       const int e = tid + 256 * s;
-      L.g.A[buf][e / 64][e % 64] = ra[s];
-      L.g.B[buf][e % 16][e / 16] = rb[s];
+      if (e < H1LEN / 4) reinterpret_cast<float4*>(h)[e] = rh[s];
     }
   };
-  __syncthreads();
-  mfma_f32x4 acc[2][2];
-  mfma_zero<2>(acc);
-  float ra[4], rb[4];
-  load(0, ra, rb);
-  store(0, ra, rb);
-  __syncthreads();
-  constexpr int NK = (K2 + MBK - 1) / MBK;
-  for (int kt = 0; kt < NK; ++kt) {
-    const int cbuf = kt & 1;
-    if (kt + 1 < NK) load((kt + 1) * MBK, ra, rb);
-    mfma_slice<2>(L.g, cbuf, wm, wn, lane, acc);
-    if (kt + 1 < NK) store(cbuf ^ 1, ra, rb);
-    __syncthreads();
+  int64_t b = blockIdx.x;
+  if (b < nB) {
+    fetch(b);
+    stage(L.h1[0]);
   }
-  // bias, then the 2 x 2 pooling of every filter's 8 x 8 map
-  const float* b2 = a.w + a.off_c2 + NC2 * K2;
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = wm * 32 + mt * 16 + 4 * (lane >> 4) + r;
-        const int o = wn * 32 + nt * 16 + (lane & 15);
-        if (o < NC2) L.z[m][o] = acc[mt][nt][r] + b2[o];
-      }
   __syncthreads();
-  for (int f = tid; f < FEAT; f += 256) {
-    const int o = f / NQ2, q = f % NQ2, y = 2 * (q / Q2), x = 2 * (q % Q2);
-    float best = L.z[y * O2 + x][o];
-    int code = 0;
-    const float z1 = L.z[y * O2 + x + 1][o], z2 = L.z[(y + 1) * O2 + x][o], z3 = L.z[(y + 1) * O2 + x + 1][o];
-    if (z1 > best) { best = z1; code = 1; }
-    if (z2 > best) { best = z2; code = 2; }
-    if (z3 > best) { best = z3; code = 3; }
-    a.F[b * FEAT + f] = best > 0.f ? best : 0.f;
-    a.code2[b * FEAT + f] = static_cast<uint8_t>(code);
+  for (int it = 0; b < nB; b += gridDim.x, ++it) {
+    const int cur = it & 1;
+    if (b + gridDim.x < nB) fetch(b + gridDim.x);
+    mfma_f32x4 acc[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) acc[mt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+    const float* h = L.h1[cur] + abase;
+#pragma unroll
+    for (int t = 0; t < 25; ++t)
+#pragma unroll
+      for (int cq = 0; cq < 5; ++cq) {
+        const int off = 4 * cq * NPOS1 + (t / 5) * Q1 + t % 5;
+        float av[4];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) av[mt] = h[off + 2 * mt * Q1];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], wb[5 * t + cq], acc[mt], 0, 0, 0);
+        if (cq == 4) __builtin_amdgcn_sched_barrier(0);   // bounds how far LDS reads run ahead
+      }
+    // acc[mt][r] = Z[m = 16 mt + 4 g + r][o = 16 wv + j]
+    if (o_mine < NC2)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) L.z[cur][16 * mt + 4 * g + r][o_mine] = acc[mt][r] + bias;
+    if (b + gridDim.x < nB) stage(L.h1[cur ^ 1]);
+    __syncthreads();
+    for (int f = tid; f < FEAT; f += 256) {
+      const int o = f / NQ2, q = f % NQ2, y = 2 * (q / Q2), x = 2 * (q % Q2);
+      float best = L.z[cur][y * O2 + x][o];
+      int code = 0;
+      const float z1 = L.z[cur][y * O2 + x + 1][o], z2 = L.z[cur][(y + 1) * O2 + x][o],
+                  z3 = L.z[cur][(y + 1) * O2 + x + 1][o];
+      if (z1 > best) { best = z1; code = 1; }
+      if (z2 > best) { best = z2; code = 2; }
+      if (z3 > best) { best = z3; code = 3; }
+      a.F[b * FEAT + f] = best > 0.f ? best : 0.f;
+      a.code2[b * FEAT + f] = static_cast<uint8_t>(best > 0.f ? code : 4);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// dP2[m][f] = (sum_h dA[m][h] Wf1[f][h]) [F[m][f] > 0]; 64 x 64 tiles.
+// dP2[m][f] = sum_h dA[m][h] Wf1[f][h]; 64 x 64 tiles.
 __global__ __launch_bounds__(256) void k_cnn_dfeat(CnnArgs a) {
   __shared__ MfmaLds<2> L;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
@@ -243,7 +268,7 @@ __global__ __launch_bounds__(256) void k_cnn_dfeat(CnnArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int64_t m = m0 + wm * 32 + mt * 16 + 4 * (lane >> 4) + r;
         const int f = n0 + wn * 32 + nt * 16 + (lane & 15);
-        if (m < nB && f < FEAT) a.dP2[m * FEAT + f] = a.F[m * FEAT + f] > 0.f ? acc[mt][nt][r] : 0.f;
+        if (m < nB && f < FEAT) a.dP2[m * FEAT + f] = acc[mt][nt][r];
       }
 }
 
@@ -332,7 +357,6 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
           }
         }
       asm volatile("" ::: "memory");   // the wave's LDS ops stay in program order
-      const float* h1 = a.H1 + b * H1LEN + c * NPOS1;
       float* dp1 = a.dP1 + b * H1LEN + c * NPOS1;
 #pragma unroll
       for (int pp = 0; pp < 3; ++pp) {
@@ -345,7 +369,7 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
           for (int u = 0; u < KS; ++u)
 #pragma unroll
             for (int v = 0; v < KS; ++v) s += src[708 * u + 143 * v];
-          dp1[p] = h1[p] > 0.f ? s : 0.f;
+          dp1[p] = s;
         }
       }
       asm volatile("" ::: "memory");
@@ -358,13 +382,15 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
 // dW2, db2 partial of chunk j of worker i (images i B + j chunk .., in order):
 // dW2[o][n] += sum_m dZ2[m][o] H1[c][m + t] with n = (c, t) = 25 c + t, a
 // 64 x 512 x 64 GEMM per image on the matrix cores (o padded to 64, n to 512;
-// the padded columns read a zero region).  Each of the four waves owns 8
+// the padded columns read a zero region, except column 500, which reads ones
+// and so collects db2).  Each of the four waves owns 8
 // column tiles and keeps its 4 x 8 accumulator tiles over the chunk; the
 // image's H1 and unpooled gradient are staged in LDS, the next image's loads
 // in flight meanwhile.
 constexpr int WG_NT = 8;                 // column tiles per wave
 constexpr int WG_ZERO = H1LEN;           // zero region after the image's H1
-constexpr int WG_H1 = H1LEN + 96;
+constexpr int WG_ONES = H1LEN + 96;      // then a region of ones
+constexpr int WG_H1 = H1LEN + 192;
 struct WgradBuf {
   float h1[WG_H1];
   float A[NPOS2 * SA_LD];                // [m][o]
@@ -375,7 +401,7 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
   const int i = blockIdx.y, jc = blockIdx.x;
   const int b0 = jc * a.chunk, b1 = min(a.B, b0 + a.chunk);
-  for (int e = tid; e < 2 * 96; e += 256) L[e / 96].h1[WG_ZERO + e % 96] = 0.f;
+  for (int e = tid; e < 2 * 192; e += 256) L[e / 192].h1[WG_ZERO + e % 192] = e % 192 < 96 ? 0.f : 1.f;
   for (int e = tid; e < 2 * NPOS2 * (SA_LD - NC2); e += 256) {
     const int bi = e / (NPOS2 * (SA_LD - NC2)), r = e % (NPOS2 * (SA_LD - NC2));
     L[bi].A[(r / (SA_LD - NC2)) * SA_LD + NC2 + r % (SA_LD - NC2)] = 0.f;
@@ -386,7 +412,7 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
   for (int nt = 0; nt < WG_NT; ++nt) {
     const int n = 16 * (WG_NT * wv + nt) + j;
     const int c = n / 25, t = n % 25;
-    colbase[nt] = (n < K2 ? c * NPOS1 + (t / 5) * Q1 + t % 5 : WG_ZERO) + g;
+    colbase[nt] = (n < K2 ? c * NPOS1 + (t / 5) * Q1 + t % 5 : n == K2 ? WG_ONES : WG_ZERO) + g;
   }
   float4 rh[3];
   float rg[4];
@@ -428,7 +454,6 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int nt = 0; nt < WG_NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  float db = 0.f;
   if (b0 < b1) {
     fetch((int64_t)i * a.B + b0);
     stage(L[0]);
@@ -438,11 +463,6 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
     const int cur = (bb - b0) & 1;
     const int64_t b = (int64_t)i * a.B + bb;
     if (bb + 1 < b1) fetch(b + 1);
-    if (tid < NC2) {
-      float s = 0.f;
-      for (int q = 0; q < NQ2; ++q) s += a.dP2[b * FEAT + tid * NQ2 + q];
-      db += s;
-    }
     const float* A = L[cur].A + g * SA_LD + j;
     const float* H = L[cur].h1;
 #pragma unroll
@@ -473,49 +493,132 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int o = 16 * mt + 4 * g + r;
-        if (o < NC2 && n < K2) p[o * K2 + n] = acc[mt][nt][r];
+        if (o < NC2 && n <= K2) p[n < K2 ? o * K2 + n : NC2 * K2 + o] = acc[mt][nt][r];
       }
     }
-  if (tid < NC2) p[NC2 * K2 + tid] = db;
 }
 
 // ---------------------------------------------------------------------------
-// dW1, db1 partial of chunk j of worker i.
-__global__ __launch_bounds__(512) void k_cnn_conv1_wgrad(CnnArgs a) {
-  __shared__ float sx[IMG * IMG];
-  __shared__ float sg[H1LEN];
-  __shared__ uint8_t scode[H1LEN];
-  const int tid = threadIdx.x;
-  const int i = blockIdx.y, j = blockIdx.x;
-  const bool active = tid < W1LEN;
-  const int o = active ? tid / 25 : 0, uv = active ? tid % 25 : 0, u = uv / 5, v = uv % 5;
-  float acc = 0.f, db = 0.f;
-  const int b0 = j * a.chunk, b1 = min(a.B, b0 + a.chunk);
-  for (int bb = b0; bb < b1; ++bb) {
-    const int64_t b = (int64_t)i * a.B + bb;
+// dW1, db1 partial of chunk j of worker i: dW1[o][t] += sum_m dZ1[o][m]
+// X[m + t] over the 24 x 24 conv1 outputs m of each image, a GEMM (filters x
+// taps, K = positions) on the matrix cores.  K runs over (pooled position p,
+// window offset d): the lanes of group d = lane / 16 take the pooled gradient
+// of p where the window's code is d and 0 elsewhere, which is the unpooled
+// dZ1.  Tap column 25 is all ones, so it collects db1.  Each wave takes a
+// quarter of the pooled positions; the four partial tiles are summed in wave
+// order at the end.
+constexpr int C1_LD = NPOS1 + 1;         // bank spread of the [o][p] rows
+struct Wg1Buf {
+  float x[IMG * IMG];
+  float g[NC1 * C1_LD];
+  uint8_t cd[NC1 * C1_LD];
+};
+
+__global__ __launch_bounds__(256) void k_cnn_conv1_wgrad(CnnArgs a) {
+  __shared__ __align__(16) Wg1Buf L[2];
+  __shared__ float red[4][32][33];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
+  const int i = blockIdx.y, jc = blockIdx.x;
+  const int b0 = jc * a.chunk, b1 = min(a.B, b0 + a.chunk);
+  // B operand of lane (d = g, tap t = 16 nt + j): X[(2 py + d / 2 + u) 28 + 2 px + d % 2 + v]
+  int xb[2];
+  float bconst[2];
+  bool bx[2];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    const int t = 16 * nt + j;
+    bx[nt] = t < 25;
+    xb[nt] = t < 25 ? ((g >> 1) + t / 5) * IMG + (g & 1) + t % 5 : 0;
+    bconst[nt] = t == 25 ? 1.f : 0.f;
+  }
+  float4 rx, rg[3];
+  uint32_t rc[3];
+  auto fetch = [&](int64_t b) {
     const int64_t row = cnn_row(a, b, false);
-    for (int e = tid; e < IMG * IMG; e += blockDim.x) sx[e] = row >= 0 ? a.X[row * (IMG * IMG) + e] : 0.f;
-    for (int e = tid; e < H1LEN; e += blockDim.x) {
-      sg[e] = a.dP1[b * H1LEN + e];
-      scode[e] = a.code1[b * H1LEN + e];
+    rx = tid < IMG * IMG / 4 && row >= 0 ? reinterpret_cast<const float4*>(a.X + row * (IMG * IMG))[tid]
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int e = tid + 256 * s;
+      rg[s] = e < H1LEN / 4 ? reinterpret_cast<const float4*>(a.dP1 + b * H1LEN)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+      rc[s] = e < H1LEN / 4 ? reinterpret_cast<const uint32_t*>(a.code1 + b * H1LEN)[e] : 0u;
     }
-    __syncthreads();
-    if (active) {
-      const float* g = sg + o * NPOS1;
-      const uint8_t* cd = scode + o * NPOS1;
-      const float* xs = sx + u * IMG + v;
-      for (int p = 0; p < NPOS1; ++p) {
-        const int y = 2 * (p / Q1) + (cd[p] >> 1), x = 2 * (p % Q1) + (cd[p] & 1);
-        acc = fmaf(g[p], xs[y * IMG + x], acc);
-        if (uv == 0) db += g[p];
+  };
+  auto stage = [&](Wg1Buf& B) {
+    if (tid < IMG * IMG / 4) reinterpret_cast<float4*>(B.x)[tid] = rx;
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int e = tid + 256 * s;
+      if (e < H1LEN / 4) {
+        const int o = (4 * e) / NPOS1, p = (4 * e) % NPOS1;   // 144 % 4 == 0: one row
+        float* gd = B.g + o * C1_LD + p;
+        uint8_t* cd = B.cd + o * C1_LD + p;
+        gd[0] = rg[s].x; gd[1] = rg[s].y; gd[2] = rg[s].z; gd[3] = rg[s].w;
+        cd[0] = rc[s] & 0xff; cd[1] = (rc[s] >> 8) & 0xff; cd[2] = (rc[s] >> 16) & 0xff; cd[3] = rc[s] >> 24;
       }
     }
+  };
+  mfma_f32x4 acc[2][2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+  // A operand row o = 16 mt + j (filters 20 .. 31 read row 0 and contribute 0)
+  int arow[2];
+  bool aval[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    aval[mt] = 16 * mt + j < NC1;
+    arow[mt] = aval[mt] ? (16 * mt + j) * C1_LD : 0;
+  }
+  if (b0 < b1) {
+    fetch((int64_t)i * a.B + b0);
+    stage(L[0]);
+  }
+  __syncthreads();
+  constexpr int PW = NPOS1 / 4;          // pooled positions per wave
+  for (int bb = b0; bb < b1; ++bb) {
+    const int cur = (bb - b0) & 1;
+    const int64_t b = (int64_t)i * a.B + bb;
+    if (bb + 1 < b1) fetch(b + 1);
+    const Wg1Buf& B = L[cur];
+#pragma unroll 4
+    for (int pi = 0; pi < PW; ++pi) {
+      const int p = PW * wv + pi, py = p / Q1, px = p % Q1;
+      const int poff = 2 * py * IMG + 2 * px;
+      float av[2], bv[2];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const float gv = B.g[arow[mt] + p];
+        const int cv = B.cd[arow[mt] + p];
+        av[mt] = aval[mt] && cv == g ? gv : 0.f;
+      }
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) bv[nt] = bx[nt] ? B.x[xb[nt] + poff] : bconst[nt];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+    }
+    if (bb + 1 < b1) stage(L[cur ^ 1]);
     __syncthreads();
   }
-  // partial [i][j][W1 (20 x 25) | b1 (20)]
-  float* p = a.part1 + ((int64_t)i * gridDim.x + j) * (W1LEN + NC1);
-  if (active) p[tid] = acc;
-  if (active && uv == 0) p[W1LEN + o] = db;
+  // acc[mt][nt][r] = (o = 16 mt + 4 g + r, t = 16 nt + j)
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wv][16 * mt + 4 * g + r][16 * nt + j] = acc[mt][nt][r];
+  __syncthreads();
+  // partial [i][jc][W1 (20 x 25) | b1 (20)]
+  float* part = a.part1 + ((int64_t)i * gridDim.x + jc) * (W1LEN + NC1);
+  for (int e = tid; e < NC1 * 26; e += 256) {
+    const int o = e / 26, t = e % 26;
+    const float s = ((red[0][o][t] + red[1][o][t]) + red[2][o][t]) + red[3][o][t];
+    part[t < 25 ? o * 25 + t : W1LEN + o] = s;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -542,7 +645,8 @@ int cnn_chunks(int B) { return (B + kCnnChunk - 1) / kCnnChunk; }
 hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t s) {
   const int64_t nB = (int64_t)a.n * a.B;
   hipLaunchKernelGGL(k_cnn_conv1_pool, dim3(static_cast<unsigned>((nB * NPOS1 + 255) / 256)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_cnn_conv2_pool, dim3(static_cast<unsigned>(nB)), dim3(256), 0, s, a);
+  const int64_t cv_blocks = nB < kConvBlocks ? nB : kConvBlocks;
+  hipLaunchKernelGGL(k_cnn_conv2_pool, dim3(static_cast<unsigned>(cv_blocks)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the fully connected part: the MLP 800-H-C on the features, its G block
@@ -559,7 +663,7 @@ hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t 
   hipLaunchKernelGGL(k_cnn_conv2_dgrad, dim3(static_cast<unsigned>(dg_blocks)), dim3(256), 0, s, a);
   const int chunks = cnn_chunks(a.B);
   hipLaunchKernelGGL(k_cnn_conv2_wgrad, dim3(chunks, a.n), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_cnn_conv1_wgrad, dim3(chunks, a.n), dim3(512), 0, s, a);
+  hipLaunchKernelGGL(k_cnn_conv1_wgrad, dim3(chunks, a.n), dim3(256), 0, s, a);
   constexpr int LW = W1LEN + NC1 + NC2 * K2 + NC2;
   hipLaunchKernelGGL(k_cnn_wreduce, dim3((LW + 255) / 256, a.n), dim3(256), 0, s, a, chunks);
   return hipGetLastError();
