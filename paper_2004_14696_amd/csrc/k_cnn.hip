@@ -310,20 +310,39 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
       }
   float* D = sD[wv];
   const int64_t nB = (int64_t)a.n * a.B;
+  // the pooled gradient and codes of the block's next image, loaded while the
+  // current one is multiplied
+  float pg[4];
+  uint32_t pc = 0;                       // four codes, a byte each
+  auto fetch = [&](int64_t bn) {
+    pc = 0;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      const bool ok = e < FEAT && bn < nB;
+      pg[s] = ok ? a.dP2[bn * FEAT + e] : 0.f;
+      pc |= static_cast<uint32_t>(ok ? a.code2[bn * FEAT + e] : 4) << (8 * s);
+    }
+  };
+  fetch(blockIdx.x);
   for (int64_t b = blockIdx.x; b < nB; b += gridDim.x) {
     // unpool: task (o, q) writes the four entries of its window in row o
-    for (int e = tid; e < FEAT; e += 256) {
-      const int o = e / NQ2, q = e % NQ2;
-      const float gv = a.dP2[b * FEAT + e];
-      const int cd = a.code2[b * FEAT + e];
-      const int m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
-      float* row = sA + o * SA_LD + m0;
-      row[0] = cd == 0 ? gv : 0.f;
-      row[1] = cd == 1 ? gv : 0.f;
-      row[O2] = cd == 2 ? gv : 0.f;
-      row[O2 + 1] = cd == 3 ? gv : 0.f;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = tid + 256 * s;
+      if (e < FEAT) {
+        const int o = e / NQ2, q = e % NQ2;
+        const int m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
+        float* row = sA + o * SA_LD + m0;
+        const uint32_t cd = (pc >> (8 * s)) & 0xff;
+        row[0] = cd == 0 ? pg[s] : 0.f;
+        row[1] = cd == 1 ? pg[s] : 0.f;
+        row[O2] = cd == 2 ? pg[s] : 0.f;
+        row[O2 + 1] = cd == 3 ? pg[s] : 0.f;
+      }
     }
     __syncthreads();
+    fetch(b + gridDim.x);
 #pragma unroll   // register index ci
     for (int ci = 0; ci < DG_CPW; ++ci) {
       const int c = DG_CPW * wv + ci;
@@ -364,13 +383,16 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
         if (p < NPOS1) {
           // framed cell of (t, y = py - u, x = px - v) = p + 52 + 708 u + 143 v
           const float* src = D + p + 52;
-          float s = 0.f;
+          float su[KS];                  // one short add chain per tap row
 #pragma unroll
-          for (int u = 0; u < KS; ++u)
+          for (int u = 0; u < KS; ++u) {
+            su[u] = src[708 * u];
 #pragma unroll
-            for (int v = 0; v < KS; ++v) s += src[708 * u + 143 * v];
-          dp1[p] = s;
+            for (int v = 1; v < KS; ++v) su[u] += src[708 * u + 143 * v];
+          }
+          dp1[p] = ((su[0] + su[1]) + (su[2] + su[3])) + su[4];
         }
+        __builtin_amdgcn_sched_barrier(0);   // at most one target's reads in flight
       }
       asm volatile("" ::: "memory");
     }
