@@ -184,6 +184,12 @@ def maxpool2(Z: np.ndarray):
     return np.take_along_axis(win, code[None], axis=0)[0], code
 
 
+def pool_take(Z: np.ndarray, code: np.ndarray):
+    """The entries of each 2 x 2 window that the codes name."""
+    win = np.stack([Z[:, :, 0::2, 0::2], Z[:, :, 0::2, 1::2], Z[:, :, 1::2, 0::2], Z[:, :, 1::2, 1::2]])
+    return np.take_along_axis(win, code[None], axis=0)[0]
+
+
 def maxpool2_grad(dP: np.ndarray, code: np.ndarray):
     """The pooled gradient placed at each window's passing entry."""
     B, Ch, h, wd = dP.shape
@@ -194,13 +200,22 @@ def maxpool2_grad(dP: np.ndarray, code: np.ndarray):
 
 
 def cnn_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: int,
-                     return_preact: bool = False):
+                     return_preact: bool = False, decisions: dict | None = None):
     """The CNN above.  Xt [n][B][784] (row-major 28 x 28 images).  Returns
     G [n][P] flattened like w, loss [n] and, on request, per worker the
     values its decisions were taken on: {"Z1": conv1 outputs [B][20][24][24],
     "Z2": conv2 outputs [B][50][8][8], "A3": first fully connected layer's
-    pre-activations [B][H]}."""
+    pre-activations [B][H]}.
+
+    decisions (n = 1 only) replaces the network's own discrete choices by
+    given ones, for tests that accept either outcome of a choice taken within
+    rounding: "code1" [B][20][12][12] and "code2" [B][50][4][4] name each
+    window's passing entry, "on1", "on2" (same shapes) and "on3" [B][H] say
+    which ReLUs pass.  The network is then the same composition with those
+    selections fixed (a pooled value is the named entry of its window)."""
     n, B, d = Xt.shape
+    dcs = decisions or {}
+    assert not dcs or n == 1
     assert d == CNN_IMG * CNN_IMG
     Wc1, bc1, Wc2, bc2, Wf1, bf1, Wf2, bf2 = cnn_split(w, H, C)
     G = np.empty((n, w.size))
@@ -211,13 +226,21 @@ def cnn_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: i
         y = np.asarray(yt[i], dtype=np.int64)
         Z1, cols1 = conv_valid(X, Wc1, bc1)                  # [B][20][24][24]
         P1, code1 = maxpool2(Z1)                             # [B][20][12][12]
-        H1 = np.where(P1 > 0.0, P1, 0.0)
+        if "code1" in dcs:
+            code1 = dcs["code1"]
+            P1 = pool_take(Z1, code1)
+        on1 = dcs.get("on1", P1 > 0.0)
+        H1 = np.where(on1, P1, 0.0)
         Z2, cols2 = conv_valid(H1, Wc2, bc2)                 # [B][50][8][8]
         P2, code2 = maxpool2(Z2)                             # [B][50][4][4]
-        H2 = np.where(P2 > 0.0, P2, 0.0)
+        if "code2" in dcs:
+            code2 = dcs["code2"]
+            P2 = pool_take(Z2, code2)
+        on2 = dcs.get("on2", P2 > 0.0)
+        H2 = np.where(on2, P2, 0.0)
         F = H2.reshape(B, CNN_FEAT)
         A3 = F @ Wf1 + bf1
-        on3 = A3 > 0.0
+        on3 = dcs.get("on3", A3 > 0.0)
         H3 = np.where(on3, A3, 0.0)
         Pr, ce = _softmax_ce(H3 @ Wf2 + bf2, y)
         R = (Pr - _onehot(y, C)) / B
@@ -227,11 +250,11 @@ def cnn_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: i
         dWf1 = F.T @ dA3
         dbf1 = dA3.sum(axis=0)
         dH2 = (dA3 @ Wf1.T).reshape(P2.shape)
-        dZ2 = maxpool2_grad(dH2 * (P2 > 0.0), code2)
+        dZ2 = maxpool2_grad(dH2 * on2, code2)
         dWc2 = conv_weight_grad(dZ2, cols2, Wc2.shape)
         dbc2 = dZ2.sum(axis=(0, 2, 3))
         dH1 = conv_input_grad(dZ2, Wc2, P1.shape[2], P1.shape[3])
-        dZ1 = maxpool2_grad(dH1 * (P1 > 0.0), code1)
+        dZ1 = maxpool2_grad(dH1 * on1, code1)
         dWc1 = conv_weight_grad(dZ1, cols1, Wc1.shape)
         dbc1 = dZ1.sum(axis=(0, 2, 3))
         G[i] = np.concatenate([dWf1.ravel(), dbf1, dWf2.ravel(), dbf2,

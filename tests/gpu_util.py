@@ -141,3 +141,82 @@ def masked_rel_err(a, o, mask) -> float:
     a = np.asarray(a, dtype=np.float64)[mask]
     o = np.asarray(o, dtype=np.float64)[mask]
     return rel_err(a, o)
+
+
+def cnn_blocks(H, C):
+    """[start, end) of the CNN's parameter blocks in G: Wf1, bf1, Wf2, bf2,
+    Wc1, bc1, Wc2, bc2."""
+    b = np.cumsum([0, 800 * H, H, H * C, C, 500, 20, 25000, 50])
+    return list(zip(b[:-1], b[1:]))
+
+
+def cnn_decision_flips(dec, frac=1e-6, conv_frac=2e-7):
+    """The choices of one worker's network that fp32 rounding could take the
+    other way, from the oracle's fp64 values (cnn_worker_grads with
+    return_preact): another entry of a pooling window within conv_frac x the
+    layer's largest magnitude of the window's largest (exactly equal entries
+    are decided alike on both sides and are not listed), a pooled value that
+    close to zero (its ReLU), a first fully connected unit with |A3| below
+    frac x max|A3|.  Returns [(image, key, index, other choice)] with the keys
+    of cnn_worker_grads' decisions."""
+    from oracle import model as omodel
+
+    out = []
+    for layer, Z in ((1, dec["Z1"]), (2, dec["Z2"])):
+        tol = conv_frac * float(np.max(np.abs(Z)))
+        win = np.stack([Z[:, :, 0::2, 0::2], Z[:, :, 0::2, 1::2], Z[:, :, 1::2, 0::2], Z[:, :, 1::2, 1::2]])
+        P, _ = omodel.maxpool2(Z)
+        for a, b, o, py, px in np.argwhere((P[None] - win <= tol) & (win != P[None])):
+            out.append((int(b), f"code{layer}", (int(o), int(py), int(px)), int(a)))
+        for b, o, py, px in np.argwhere(np.abs(P) <= tol):
+            out.append((int(b), f"on{layer}", (int(o), int(py), int(px)), not bool(P[b, o, py, px] > 0)))
+    A = dec["A3"]
+    for b, u in np.argwhere(np.abs(A) < frac * float(np.max(np.abs(A)))):
+        out.append((int(b), "on3", (int(u),), not bool(A[b, u] > 0)))
+    return out
+
+
+def cnn_flip_deltas(w, X, y, H, C, dec, flips):
+    """Per flip, the oracle's change of the worker gradient (the mean over its
+    B images) when that one choice goes the other way: the flip's image
+    alone, run with all its other choices as the network's own.  X [B][784],
+    y [B]."""
+    from oracle import model as omodel
+
+    B = X.shape[0]
+    w = np.asarray(w, dtype=np.float64)
+    base, deltas = {}, []
+    for b, key, idx, val in flips:
+        if b not in base:
+            P1, c1 = omodel.maxpool2(dec["Z1"][b:b + 1])
+            P2, c2 = omodel.maxpool2(dec["Z2"][b:b + 1])
+            own = {"code1": c1, "on1": P1 > 0, "code2": c2, "on2": P2 > 0, "on3": dec["A3"][b:b + 1] > 0}
+            g = omodel.cnn_worker_grads(w, X[b][None, None], y[b][None, None], H, C, decisions=own)[0][0]
+            base[b] = (own, g)
+        own, g0 = base[b]
+        alt = dict(own)
+        alt[key] = own[key].copy()
+        alt[key][(0, *idx)] = val
+        g = omodel.cnn_worker_grads(w, X[b][None, None], y[b][None, None], H, C, decisions=alt)[0][0]
+        if np.any(g != g0):
+            deltas.append((g - g0) / B)
+    return deltas
+
+
+def cnn_best_flip_err(a, o, deltas, H, C, limit=12) -> float:
+    """The largest per-block relative error max|a - o'| / max|o'| over the
+    CNN's parameter blocks, minimised over o' = o plus the sum of any subset
+    of the flips' deltas (each choice within rounding may go either way)."""
+    assert len(deltas) <= limit, len(deltas)
+    a = np.asarray(a, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    best = np.inf
+    for m in range(1 << len(deltas)):
+        ref = o.copy()
+        for i, d in enumerate(deltas):
+            if m >> i & 1:
+                ref += d
+        err = max(float(np.max(np.abs(a[lo:hi] - ref[lo:hi]))) / max(float(np.max(np.abs(ref[lo:hi]))), 1e-30)
+                  for lo, hi in cnn_blocks(H, C))
+        best = min(best, err)
+    return best

@@ -11,8 +11,8 @@ from oracle import dbw as odbw
 from oracle import model as omodel
 from oracle import ps as ops
 
-from gpu_util import (RTOL, cnn_compare_mask, host, k_acceptable, masked_rel_err, mlp_compare_mask, mlp_inputs, rel_err,
-                      scalar_rel, softmax_inputs, to_dev)
+from gpu_util import (RTOL, cnn_best_flip_err, cnn_decision_flips, cnn_flip_deltas, host,
+                      k_acceptable, masked_rel_err, mlp_compare_mask, mlp_inputs, rel_err, scalar_rel, softmax_inputs, to_dev)
 
 torch = pytest.importorskip("torch")
 pb = pytest.importorskip("paper_2004_14696_amd.binding")
@@ -189,11 +189,12 @@ def test_worker_grads_cnn(n, B, H, C):
     G, loss = ctx.worker_grads(to_dev(torch, w), to_dev(torch, X), to_dev(torch, y))
     ctx.sync()
     Go, lo, dec = omodel.cnn_worker_grads(w.astype(np.float64), X, y, H, C, return_preact=True)
-    masks, amb, conv_out = cnn_compare_mask(dec, H, C)
-    assert conv_out <= n // 2, (amb, conv_out)       # decisions within rounding are rare
     Gg = host(G)
     for i in range(n):
-        assert masked_rel_err(Gg[i], Go[i], masks[i]) <= RTOL, i
+        # every parameter block against its own largest entry; a choice that
+        # rounding could take either way is accepted both ways
+        deltas = cnn_flip_deltas(w, X[i], y[i], H, C, dec[i], cnn_decision_flips(dec[i]))
+        assert cnn_best_flip_err(Gg[i], Go[i], deltas, H, C) <= RTOL, (i, len(deltas))
     assert rel_err(host(loss), lo) <= RTOL
 
 
@@ -213,8 +214,11 @@ def test_worker_grads_cnn_workload_shape_sampled_workers():
     for i in (0, 7, 15):
         Go, lo, dec = omodel.cnn_worker_grads(w.astype(np.float64), Xs[idx[i]][None], ys[idx[i]][None], H, C,
                                               return_preact=True)
-        masks, amb, conv_out = cnn_compare_mask(dec, H, C)
-        assert masked_rel_err(Gg[i], Go[0], masks[0]) <= RTOL, (i, amb, conv_out)
+        # every block compared (no masks): each choice within rounding (about
+        # one to five per worker here) is accepted either way
+        flips = cnn_decision_flips(dec[0])
+        deltas = cnn_flip_deltas(w, Xs[idx[i]], ys[idx[i]], H, C, dec[0], flips)
+        assert cnn_best_flip_err(Gg[i], Go[0], deltas, H, C) <= RTOL, (i, len(flips), len(deltas))
         assert lg[i] == pytest.approx(lo[0], rel=RTOL)
 
 

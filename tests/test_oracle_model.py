@@ -209,6 +209,64 @@ def test_cnn_finite_differences():
             assert G[0, p] == pytest.approx(fd, rel=1e-4, abs=tol), (lo, p, h)
 
 
+def test_cnn_fixed_decisions_match_finite_differences():
+    # With every pooling choice and ReLU fixed (some of them flipped from the
+    # network's own), the loss is a smooth function of w whose gradient the
+    # oracle must return; and its own decisions, passed in, change nothing.
+    rng = np.random.default_rng(65)
+    B, H, C = 2, 8, 4
+    X = rng.random((1, B, 784))
+    y = rng.integers(0, C, size=(1, B))
+    w = rng.uniform(-0.15, 0.15, size=model.cnn_param_count(H, C))
+    G0, L0, dec = model.cnn_worker_grads(w, X, y, H, C, return_preact=True)
+    Z1, Z2, A3 = dec[0]["Z1"], dec[0]["Z2"], dec[0]["A3"]
+    P1, code1 = model.maxpool2(Z1)
+    P2, code2 = model.maxpool2(Z2)
+    own = {"code1": code1, "on1": P1 > 0, "code2": code2, "on2": P2 > 0, "on3": A3 > 0}
+    G1, L1 = model.cnn_worker_grads(w, X, y, H, C, decisions=own)
+    np.testing.assert_array_equal(G1, G0)
+    assert L1[0] == L0[0]
+    flip = {k: v.copy() for k, v in own.items()}
+    flip["code1"][0, 3, 5, 6] = (code1[0, 3, 5, 6] + 1) % 4
+    flip["on1"][1, 7, 2, 2] = ~own["on1"][1, 7, 2, 2]
+    j = np.argwhere(own["on2"][0])[0]                  # a passing conv2 window
+    flip["code2"][0][tuple(j)] = (code2[0][tuple(j)] + 2) % 4
+    flip["on2"][1, 10, 1, 3] = ~own["on2"][1, 10, 1, 3]
+    flip["on3"][0, 2] = ~own["on3"][0, 2]
+    G, L = model.cnn_worker_grads(w, X, y, H, C, decisions=flip)
+    bounds = np.cumsum([0, 800 * H, H, H * C, C, 500, 20, 25000, 50])
+    # each override on its own moves the gradient where it must
+    for key, idx, lo, hi in (("code1", (0, 3, 5, 6), bounds[4] + 75, bounds[4] + 100),
+                             ("on1", (1, 7, 2, 2), bounds[4] + 175, bounds[4] + 200),
+                             ("code2", (0, *j), bounds[6] + j[0] * 500, bounds[6] + j[0] * 500 + 500),
+                             ("on2", (1, 10, 1, 3), bounds[7] + 10, bounds[7] + 11),
+                             ("on3", (0, 2), bounds[1] + 2, bounds[1] + 3)):
+        one = dict(own)
+        one[key] = own[key].copy()
+        one[key][idx] = flip[key][idx]
+        Gk = model.cnn_worker_grads(w, X, y, H, C, decisions=one)[0]
+        assert not np.array_equal(Gk[0, lo:hi], G0[0, lo:hi]), key
+
+    def loss_at(v):
+        return model.cnn_worker_grads(v, X, y, H, C, decisions=flip)[1][0]
+
+    # every conv1 weight and every bias; in the large blocks random entries
+    # plus those the flips touch (conv2 filter j[0], the first layer's unit 2)
+    check = [np.arange(bounds[4], bounds[6]), np.arange(bounds[7], bounds[8]),
+             np.arange(bounds[1], bounds[2]), np.arange(bounds[3], bounds[4]),
+             rng.choice(np.arange(bounds[0], bounds[1]), 12, replace=False),
+             np.arange(2, 800 * H, H)[rng.choice(800, 12, replace=False)],
+             rng.choice(np.arange(bounds[2], bounds[3]), 12, replace=False),
+             rng.choice(np.arange(bounds[6], bounds[7]), 12, replace=False),
+             bounds[6] + j[0] * 500 + rng.choice(500, 24, replace=False)]
+    h = 1e-5
+    for p in np.concatenate(check):
+        e = np.zeros_like(w)
+        e[p] = h
+        fd = (loss_at(w + e) - loss_at(w - e)) / (2 * h)
+        assert G[0, p] == pytest.approx(fd, rel=1e-5, abs=1e-9), p
+
+
 def test_cnn_closed_form_at_zero():
     # all parameters 0: logits 0, uniform class probabilities, loss ln C; only
     # the last bias has a gradient, the batch mean of 1/C - onehot(y)
