@@ -281,11 +281,12 @@ template <int U, int CW>
 __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs, int rps, int64_t per_xcd) {
   static_assert(CW % 2 == 0 && CW <= 16, "class padding");
   // W in lane order: lane (w, m) reads its 4U features x CW classes from one
-  // contiguous run (features w 64U + 64u + 4m + j at (4u + j) CW); the run
-  // length SL = 8a + 4 floats puts the 16 lanes of a row group on distinct
-  // bank pairs for 8-byte reads.  The same LDS later assembles the block's
-  // slice of G ([d][C]).
-  constexpr int SL = 4 * U * CW + 4;
+  // contiguous run (features w 64U + 64u + 4m + j at (4u + j) CW); with the
+  // run length SL = 4 U CW + 2 floats, SL / 2 is odd, so the 16 distinct
+  // 8-byte reads of a row group fall on distinct bank pairs of the 32 banks
+  // (runs start 8-byte aligned, so W is staged with 8-byte stores).  The same
+  // LDS later assembles the block's slice of G ([d][C]).
+  constexpr int SL = 4 * U * CW + 2;
   constexpr int WS = MF_WAVES * 16 * SL;
   __shared__ __attribute__((aligned(16))) float Ws[WS];
   __shared__ float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
@@ -360,7 +361,7 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
 
   // Stage W.  Features 4h .. 4h+3 (group h = w' 16U + 16u + m') are 4C
   // contiguous elements of W and 4CW contiguous floats of run (w', m') at
-  // 4u CW, so with C == CW the copy is float4 to float4.
+  // 4u CW, so with C == CW a float4 of W lands as two float2 stores.
   {
     // float index in Ws of element r of group h's 4CW floats
     auto slot = [](int h, int r) { return ((h / (16 * U)) * 16 + h % 16) * SL + ((h % (16 * U)) / 16) * 4 * CW + r; };
@@ -368,7 +369,11 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
 #pragma unroll
       for (int k = 0; k < KMAX; ++k) {
         const int e = 4 * (tid + k * MF_T);
-        if (e < 4 * n4) w4[slot(e / (4 * CW), e % (4 * CW)) / 4] = wl[k];
+        if (e < 4 * n4) {
+          float2* w2 = reinterpret_cast<float2*>(Ws) + slot(e / (4 * CW), e % (4 * CW)) / 2;
+          w2[0] = make_float2(wl[k].x, wl[k].y);
+          w2[1] = make_float2(wl[k].z, wl[k].w);
+        }
       }
     } else {
 #pragma unroll
