@@ -526,22 +526,25 @@ __global__ __launch_bounds__(256) void k_cnn_conv2_wgrad(CnnArgs a) {
 // taps, K = positions) on the matrix cores.  K runs over (pooled position p,
 // window offset d): the lanes of group d = lane / 16 take the pooled gradient
 // of p where the window's code is d and 0 elsewhere, which is the unpooled
-// dZ1.  Tap column 25 is all ones, so it collects db1.  Each wave takes a
-// quarter of the pooled positions; the four partial tiles are summed in wave
-// order at the end.
+// dZ1.  Tap column 25 is all ones, so it collects db1.  Each wave takes whole
+// images of the chunk (every fourth), staged in its own LDS region while the
+// next one is loaded into registers; the four waves' partial tiles are
+// summed in wave order at the end.
 constexpr int C1_LD = NPOS1 + 1;         // bank spread of the [o][p] rows
 struct Wg1Buf {
   float x[IMG * IMG];
   float g[NC1 * C1_LD];
-  uint8_t cd[NC1 * C1_LD];
+  uint8_t cd[NC1 * C1_LD + 12];
 };
+constexpr int C1_X4 = (IMG * IMG / 4 + 63) / 64;     // float4 pieces per lane
+constexpr int C1_G4 = (H1LEN / 4 + 63) / 64;
 
-__global__ __launch_bounds__(256) void k_cnn_conv1_wgrad(CnnArgs a) {
-  __shared__ __align__(16) Wg1Buf L[2];
-  __shared__ float red[4][32][33];
+__global__ __launch_bounds__(256, 2) void k_cnn_conv1_wgrad(CnnArgs a) {
+  __shared__ __align__(16) Wg1Buf L[4];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
   const int i = blockIdx.y, jc = blockIdx.x;
   const int b0 = jc * a.chunk, b1 = min(a.B, b0 + a.chunk);
+  Wg1Buf& B = L[wv];
   // B operand of lane (d = g, tap t = 16 nt + j): X[(2 py + d / 2 + u) 28 + 2 px + d % 2 + v]
   int xb[2];
   float bconst[2];
@@ -553,24 +556,40 @@ __global__ __launch_bounds__(256) void k_cnn_conv1_wgrad(CnnArgs a) {
     xb[nt] = t < 25 ? ((g >> 1) + t / 5) * IMG + (g & 1) + t % 5 : 0;
     bconst[nt] = t == 25 ? 1.f : 0.f;
   }
-  float4 rx, rg[3];
-  uint32_t rc[3];
+  // A operand row o = 16 mt + j (filters 20 .. 31 read row 0 and contribute 0)
+  int arow[2];
+  bool aval[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    aval[mt] = 16 * mt + j < NC1;
+    arow[mt] = aval[mt] ? (16 * mt + j) * C1_LD : 0;
+  }
+  float4 rx[C1_X4], rg[C1_G4];
+  uint32_t rc[C1_G4];
   auto fetch = [&](int64_t b) {
     const int64_t row = cnn_row(a, b, false);
-    rx = tid < IMG * IMG / 4 && row >= 0 ? reinterpret_cast<const float4*>(a.X + row * (IMG * IMG))[tid]
-                                         : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int s = 0; s < 3; ++s) {
-      const int e = tid + 256 * s;
+    for (int s = 0; s < C1_X4; ++s) {
+      const int e = lane + 64 * s;
+      rx[s] = e < IMG * IMG / 4 && row >= 0 ? reinterpret_cast<const float4*>(a.X + row * (IMG * IMG))[e]
+                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int s = 0; s < C1_G4; ++s) {
+      const int e = lane + 64 * s;
       rg[s] = e < H1LEN / 4 ? reinterpret_cast<const float4*>(a.dP1 + b * H1LEN)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
       rc[s] = e < H1LEN / 4 ? reinterpret_cast<const uint32_t*>(a.code1 + b * H1LEN)[e] : 0u;
     }
   };
-  auto stage = [&](Wg1Buf& B) {
-    if (tid < IMG * IMG / 4) reinterpret_cast<float4*>(B.x)[tid] = rx;
+  auto stage = [&]() {
 #pragma unroll
-    for (int s = 0; s < 3; ++s) {
-      const int e = tid + 256 * s;
+    for (int s = 0; s < C1_X4; ++s) {
+      const int e = lane + 64 * s;
+      if (e < IMG * IMG / 4) reinterpret_cast<float4*>(B.x)[e] = rx[s];
+    }
+#pragma unroll
+    for (int s = 0; s < C1_G4; ++s) {
+      const int e = lane + 64 * s;
       if (e < H1LEN / 4) {
         const int o = (4 * e) / NPOS1, p = (4 * e) % NPOS1;   // 144 % 4 == 0: one row
         float* gd = B.g + o * C1_LD + p;
@@ -585,48 +604,44 @@ __global__ __launch_bounds__(256) void k_cnn_conv1_wgrad(CnnArgs a) {
   for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  // A operand row o = 16 mt + j (filters 20 .. 31 read row 0 and contribute 0)
-  int arow[2];
-  bool aval[2];
+  int bb = b0 + wv;
+  if (bb < b1) fetch((int64_t)i * a.B + bb);
+  for (; bb < b1; bb += 4) {
+    stage();
+    asm volatile("" ::: "memory");       // the wave's LDS writes precede its reads
+    if (bb + 4 < b1) fetch((int64_t)i * a.B + bb + 4);
+    // pooled row py, column px: every read is unconditional (padding lanes
+    // read valid cells and select), offsets are immediates within a row
+#pragma unroll 1
+    for (int py = 0; py < Q1; ++py) {
+      const float* gr0 = B.g + arow[0] + py * Q1;
+      const float* gr1 = B.g + arow[1] + py * Q1;
+      const uint8_t* cr0 = B.cd + arow[0] + py * Q1;
+      const uint8_t* cr1 = B.cd + arow[1] + py * Q1;
+      const float* xr0 = B.x + xb[0] + 2 * py * IMG;
+      const float* xr1 = B.x + xb[1] + 2 * py * IMG;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-    aval[mt] = 16 * mt + j < NC1;
-    arow[mt] = aval[mt] ? (16 * mt + j) * C1_LD : 0;
-  }
-  if (b0 < b1) {
-    fetch((int64_t)i * a.B + b0);
-    stage(L[0]);
-  }
-  __syncthreads();
-  constexpr int PW = NPOS1 / 4;          // pooled positions per wave
-  for (int bb = b0; bb < b1; ++bb) {
-    const int cur = (bb - b0) & 1;
-    const int64_t b = (int64_t)i * a.B + bb;
-    if (bb + 1 < b1) fetch(b + 1);
-    const Wg1Buf& B = L[cur];
-#pragma unroll 4
-    for (int pi = 0; pi < PW; ++pi) {
-      const int p = PW * wv + pi, py = p / Q1, px = p % Q1;
-      const int poff = 2 * py * IMG + 2 * px;
-      float av[2], bv[2];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const float gv = B.g[arow[mt] + p];
-        const int cv = B.cd[arow[mt] + p];
-        av[mt] = aval[mt] && cv == g ? gv : 0.f;
+      for (int px = 0; px < Q1; ++px) {
+        const float g0 = gr0[px], g1 = gr1[px];
+        const int c0 = cr0[px], c1 = cr1[px];
+        const float x0 = xr0[2 * px], x1 = xr1[2 * px];
+        const float av0 = (c0 == g) & aval[0] ? g0 : 0.f;
+        const float av1 = (c1 == g) & aval[1] ? g1 : 0.f;
+        const float bv0 = bx[0] ? x0 : bconst[0];
+        const float bv1 = bx[1] ? x1 : bconst[1];
+        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av0, bv0, acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av0, bv1, acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av1, bv0, acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av1, bv1, acc[1][1], 0, 0, 0);
       }
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) bv[nt] = bx[nt] ? B.x[xb[nt] + poff] : bconst[nt];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
     }
-    if (bb + 1 < b1) stage(L[cur ^ 1]);
-    __syncthreads();
+    asm volatile("" ::: "memory");       // reads done before the next image's writes
   }
-  // acc[mt][nt][r] = (o = 16 mt + 4 g + r, t = 16 nt + j)
+  // acc[mt][nt][r] = (o = 16 mt + 4 g + r, t = 16 nt + j); the four waves'
+  // tiles meet in the staging LDS, now free
+  __syncthreads();
+  float (*red)[32][33] = reinterpret_cast<float (*)[32][33]>(&L[0]);
+  static_assert(sizeof(float) * 4 * 32 * 33 <= sizeof(L), "reduction tiles fit in the staging LDS");
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
