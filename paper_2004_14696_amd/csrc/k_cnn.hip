@@ -293,6 +293,10 @@ constexpr int kDgradBlocks = 512;        // two blocks per CU
 __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
   __shared__ float sA[52 * SA_LD];                     // [o][m]
   __shared__ __align__(16) float sD[4][DLEN];           // per wave
+  // the next image's pooled gradient and codes, loaded straight into LDS
+  // while the current image is multiplied
+  __shared__ float rawg[FEAT];
+  __shared__ uint32_t rawc[FEAT / 4];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, j = lane & 15;
   for (int i = tid; i < 4 * DLEN; i += 256) (&sD[0][0])[i] = 0.f;
   for (int i = tid; i < 2 * SA_LD; i += 256) sA[NC2 * SA_LD + i] = 0.f;   // rows o = 50, 51
@@ -310,43 +314,39 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
       }
   float* D = sD[wv];
   const int64_t nB = (int64_t)a.n * a.B;
-  // the pooled gradient and codes of the block's next image, loaded while the
-  // current one is multiplied
-  float pg[4];
-  uint32_t pc = 0;                       // four codes, a byte each
   auto fetch = [&](int64_t bn) {
-    pc = 0;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int e = tid + 256 * s;
-      const bool ok = e < FEAT && bn < nB;
-      pg[s] = ok ? a.dP2[bn * FEAT + e] : 0.f;
-      pc |= static_cast<uint32_t>(ok ? a.code2[bn * FEAT + e] : 4) << (8 * s);
+    // wave wv copies pieces wv, wv + 4, .. of 64 dwords; lanes past the end
+    // stay idle
+    for (int k = wv; k * 64 < FEAT + FEAT / 4; k += 4) {
+      const int e = 64 * k + lane;
+      if (e < FEAT)
+        __builtin_amdgcn_global_load_lds(a.dP2 + bn * FEAT + e, rawg + 64 * k, 4, 0, 0);
+      else if (e < FEAT + FEAT / 4)
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint32_t*>(a.code2 + bn * FEAT) + (e - FEAT),
+                                         rawc + (64 * k - FEAT), 4, 0, 0);
     }
   };
-  fetch(blockIdx.x);
+  if (blockIdx.x < nB) fetch(blockIdx.x);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   for (int64_t b = blockIdx.x; b < nB; b += gridDim.x) {
     // unpool: task (o, q) writes the four entries of its window in row o
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int e = tid + 256 * s;
-      if (e < FEAT) {
-        const int o = e / NQ2, q = e % NQ2;
-        const int m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
-        float* row = sA + o * SA_LD + m0;
-        const uint32_t cd = (pc >> (8 * s)) & 0xff;
-        row[0] = cd == 0 ? pg[s] : 0.f;
-        row[1] = cd == 1 ? pg[s] : 0.f;
-        row[O2] = cd == 2 ? pg[s] : 0.f;
-        row[O2 + 1] = cd == 3 ? pg[s] : 0.f;
-      }
+    const uint8_t* rc = reinterpret_cast<const uint8_t*>(rawc);
+    for (int e = tid; e < FEAT; e += 256) {
+      const int o = e / NQ2, q = e % NQ2;
+      const int m0 = 2 * (q / Q2) * O2 + 2 * (q % Q2);
+      const float gv = rawg[e];
+      const int cd = rc[e];
+      float* row = sA + o * SA_LD + m0;
+      row[0] = cd == 0 ? gv : 0.f;
+      row[1] = cd == 1 ? gv : 0.f;
+      row[O2] = cd == 2 ? gv : 0.f;
+      row[O2 + 1] = cd == 3 ? gv : 0.f;
     }
     __syncthreads();
-    fetch(b + gridDim.x);
-#pragma unroll   // register index ci
-    for (int ci = 0; ci < DG_CPW; ++ci) {
-      const int c = DG_CPW * wv + ci;
-      mfma_f32x4 acc[4][2];
+    if (b + gridDim.x < nB) fetch(b + gridDim.x);
+    // dcols of channel ci on the matrix cores
+    auto products = [&](int ci, mfma_f32x4 (&acc)[4][2]) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
@@ -362,8 +362,10 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
           for (int nt = 0; nt < 2; ++nt)
             acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], wb[ci][nt][ks], acc[mt][nt], 0, 0, 0);
       }
-      // acc[mt][nt][r]: m = 16 mt + 4 g + r (y = 2 mt + g / 2, x = 4 (g % 2) + r),
-      // tap t = 16 nt + j
+    };
+    // acc[mt][nt][r]: m = 16 mt + 4 g + r (y = 2 mt + g / 2, x = 4 (g % 2) + r),
+    // tap t = 16 nt + j, into the framed tap maps
+    auto store = [&](const mfma_f32x4 (&acc)[4][2]) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
@@ -375,7 +377,8 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
                 make_float4(acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]);
           }
         }
-      asm volatile("" ::: "memory");   // the wave's LDS ops stay in program order
+    };
+    auto fold = [&](int c) {
       float* dp1 = a.dP1 + b * H1LEN + c * NPOS1;
 #pragma unroll
       for (int pp = 0; pp < 3; ++pp) {
@@ -392,10 +395,23 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv2_dgrad(CnnArgs a) {
           }
           dp1[p] = ((su[0] + su[1]) + (su[2] + su[3])) + su[4];
         }
-        __builtin_amdgcn_sched_barrier(0);   // at most one target's reads in flight
+        // one target's reads in flight at a time; matrix-core work may cross
+        __builtin_amdgcn_sched_barrier(0x8);
       }
+    };
+    // channel ci + 1's products run while channel ci is folded: they need
+    // neither its maps nor its results
+    mfma_f32x4 acc[4][2];
+    products(0, acc);
+#pragma unroll   // register index ci
+    for (int ci = 0; ci < DG_CPW; ++ci) {
+      store(acc);
+      asm volatile("" ::: "memory");   // the wave's LDS ops stay in program order
+      if (ci + 1 < DG_CPW) products(ci + 1, acc);
+      fold(DG_CPW * wv + ci);
       asm volatile("" ::: "memory");
     }
+    __builtin_amdgcn_s_waitcnt(0);   // the next image's copy has landed
     __syncthreads();
   }
 }
