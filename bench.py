@@ -37,6 +37,7 @@ TRAFFIC_FILE = {
     "C3": "profiles/traffic_worker_grads_softmax_n64_B256_d3072_C10.md",
     "C4": "profiles/traffic_worker_grads_mlp_n32_B64_784_512_10.md",
     "C5": "profiles/traffic_worker_grads_softmax_n256_B512_d3072_C100.md",
+    "C6": "profiles/traffic_worker_grads_cnn_n16_B500_28x28_H500_C10.md",
 }
 
 
