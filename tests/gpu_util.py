@@ -95,48 +95,6 @@ def mlp_compare_mask(A, d, H, C, frac=1e-6):
     return masks, amb
 
 
-def cnn_compare_mask(dec, H, C, frac=1e-6, conv_frac=2e-7):
-    """Masks over the CNN's P gradient entries to compare (layout: the MLP
-    800-H-C first, then the 25570 convolution parameters).
-
-    Decisions the GPU takes in fp32 on values within rounding of the
-    threshold may go either way: a fully connected ReLU (|A3| < frac max|A3|)
-    masks that unit's column of W1 and its b1 entry, as for the MLP; a pooling
-    window whose two largest entries are within conv_frac of the layer's
-    largest magnitude (about three times the rms fp32 rounding of its 25- to
-    500-term sums), a pooled value within that of zero (its ReLU), or an ambiguous
-    fully connected unit (it feeds the features' gradient) masks the worker's
-    whole convolution block; an exact tie is decided alike on both sides.  Returns (masks, ambiguous units, workers whose
-    convolution block is masked)."""
-    n = len(dec)
-    d = 800
-    mlp = d * H + H + H * C + C
-    P = mlp + 25570
-    masks = np.ones((n, P), dtype=bool)
-    amb = conv_out = 0
-    for i, z in enumerate(dec):
-        A = z["A3"]
-        units = np.flatnonzero(np.any(np.abs(A) < frac * float(np.max(np.abs(A))), axis=0))
-        amb += units.size
-        for u in units:
-            masks[i, u:d * H:H] = False
-            masks[i, d * H + u] = False
-        unclear = units.size > 0
-        for Z in (z["Z1"], z["Z2"]):
-            tau = conv_frac * float(np.max(np.abs(Z)))
-            win = np.sort(np.stack([Z[:, :, 0::2, 0::2], Z[:, :, 0::2, 1::2],
-                                    Z[:, :, 1::2, 0::2], Z[:, :, 1::2, 1::2]]), axis=0)
-            # an exact tie (windows over blank input: every entry is the bias,
-            # exactly, on both sides) is decided alike; a gap within rounding
-            # is not
-            gap = win[3] - win[2]
-            unclear |= bool(np.any((gap > 0) & (gap < tau))) or bool(np.any(np.abs(win[3]) < tau))
-        if unclear:
-            masks[i, mlp:] = False
-            conv_out += 1
-    return masks, amb, conv_out
-
-
 def masked_rel_err(a, o, mask) -> float:
     a = np.asarray(a, dtype=np.float64)[mask]
     o = np.asarray(o, dtype=np.float64)[mask]
@@ -203,14 +161,15 @@ def cnn_flip_deltas(w, X, y, H, C, dec, flips):
     return deltas
 
 
-def cnn_best_flip_err(a, o, deltas, H, C, limit=12) -> float:
-    """The largest per-block relative error max|a - o'| / max|o'| over the
-    CNN's parameter blocks, minimised over o' = o plus the sum of any subset
-    of the flips' deltas (each choice within rounding may go either way)."""
+def cnn_best_flip(a, o, deltas, H, C, limit=12):
+    """o' = o plus the sum of the subset of the flips' deltas (each choice
+    within rounding may go either way) that minimises the largest per-block
+    relative error max|a - o'| / max|o'| over the CNN's parameter blocks.
+    Returns (that error, o')."""
     assert len(deltas) <= limit, len(deltas)
     a = np.asarray(a, dtype=np.float64)
     o = np.asarray(o, dtype=np.float64)
-    best = np.inf
+    best, best_ref = np.inf, o
     for m in range(1 << len(deltas)):
         ref = o.copy()
         for i, d in enumerate(deltas):
@@ -218,5 +177,11 @@ def cnn_best_flip_err(a, o, deltas, H, C, limit=12) -> float:
                 ref += d
         err = max(float(np.max(np.abs(a[lo:hi] - ref[lo:hi]))) / max(float(np.max(np.abs(ref[lo:hi]))), 1e-30)
                   for lo, hi in cnn_blocks(H, C))
-        best = min(best, err)
-    return best
+        if err < best:
+            best, best_ref = err, ref
+    return best, best_ref
+
+
+def cnn_best_flip_err(a, o, deltas, H, C, limit=12) -> float:
+    """The error of cnn_best_flip."""
+    return cnn_best_flip(a, o, deltas, H, C, limit)[0]
