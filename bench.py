@@ -319,7 +319,7 @@ def main(argv=None) -> int:
         },
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, iters_cap=50, budget_s=args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(cfg, iters_cap=1000, budget_s=args.cpu_budget)
     print(json.dumps(out), flush=True)
     return 0
 
