@@ -178,10 +178,11 @@ def _cnn_inputs(rng, n, B, H, C):
     return X, y, np.concatenate(parts)
 
 
-@pytest.mark.parametrize("n,B,H,C", [(3, 8, 24, 10), (2, 37, 500, 10), (5, 4, 7, 3)])
+@pytest.mark.parametrize("n,B,H,C", [(3, 8, 24, 10), (2, 37, 500, 10), (5, 4, 7, 3), (1, 1030, 16, 10)])
 def test_worker_grads_cnn(n, B, H, C):
     # ragged batches (37 rows: chunks of 16 images plus a tail), a narrow and
-    # the workload's fully connected width
+    # the workload's fully connected width; above 1024 images per worker the
+    # fully connected part takes the MLP's vector-ALU kernels
     rng = np.random.default_rng(3000 + n + B + H)
     X, y, w = _cnn_inputs(rng, n, B, H, C)
     ctx = _ctx(n, B, 784, C, model="cnn", H=H)
