@@ -80,10 +80,16 @@ def mlp_split(w: np.ndarray, d: int, H: int, C: int):
 
 
 def mlp_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: int,
-                     return_preact: bool = False):
+                     return_preact: bool = False, decisions: dict | None = None):
     """Two-layer ReLU MLP.  Returns G [n][P] (flattened like w), loss [n] and,
-    on request, the hidden pre-activations A [n][B][H] (the ReLU decisions)."""
+    on request, the hidden pre-activations A [n][B][H] (the ReLU decisions).
+
+    decisions (n = 1 only): {"on": [B][H] booleans} replaces the ReLU
+    decisions [A > 0], for tests that accept either outcome of a decision
+    taken within rounding; the network is then the same composition with
+    those units fixed on or off."""
     n, B, d = Xt.shape
+    assert not decisions or n == 1
     W1, b1, W2, b2 = mlp_split(w, d, H, C)
     P_ = w.size
     G = np.empty((n, P_))
@@ -93,7 +99,7 @@ def mlp_worker_grads(w: np.ndarray, Xt: np.ndarray, yt: np.ndarray, H: int, C: i
         X = np.asarray(Xt[i], dtype=np.float64)
         y = np.asarray(yt[i], dtype=np.int64)
         A = X @ W1 + b1
-        on = A > 0.0
+        on = decisions["on"] if decisions else A > 0.0
         Hh = np.where(on, A, 0.0)
         P, ce = _softmax_ce(Hh @ W2 + b2, y)
         R = (P - _onehot(y, C)) / B

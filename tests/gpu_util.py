@@ -72,27 +72,61 @@ def mlp_inputs(rng, n, B, d, H, C):
     return X, y, w
 
 
-def mlp_compare_mask(A, d, H, C, frac=1e-6):
-    """Per-worker boolean masks over the P gradient entries to compare.
+def mlp_decision_flips(A_i, tau):
+    """The hidden ReLUs of one worker (pre-activations A_i [B][H]) that fp32
+    rounding could decide the other way: |A| < tau, with tau = frac x the
+    largest |A| (frac 1e-6 is about 50x the rounding of a 784-term fp32 dot
+    product).  Returns [(row, unit, other decision)]."""
+    return [(int(b), int(u), not bool(A_i[b, u] > 0)) for b, u in np.argwhere(np.abs(A_i) < tau)]
 
-    The ReLU decision [A > 0] is taken in fp32 on the GPU; pre-activations
-    within fp32 rounding of zero (|A| < frac * max|A|, about 50x the rounding
-    error of a 784-term fp32 dot product) may go either way, and
-    with them the hidden unit's column of dW1 and its entry of db1.  Those
-    entries are excluded; everything else is compared.  Returns (masks, count
-    of ambiguous (worker, unit) pairs)."""
-    n = A.shape[0]
-    P = d * H + H + H * C + C
-    masks = np.ones((n, P), dtype=bool)
-    amb = 0
-    tau = frac * float(np.max(np.abs(A)))
-    for i in range(n):
-        units = np.flatnonzero(np.any(np.abs(A[i]) < tau, axis=0))
-        amb += units.size
-        for u in units:
-            masks[i, u:d * H:H] = False      # dW1[:, u]
-            masks[i, d * H + u] = False      # db1[u]
-    return masks, amb
+
+def mlp_flip_deltas(w, X, y, H, C, A_i, flips):
+    """Per flip, the oracle's change of the worker gradient (mean over its B
+    rows) when that ReLU goes the other way: the flip's row alone, all its
+    other units as the network's own.  X [B][d], y [B].  Returns [(unit,
+    delta)]."""
+    from oracle import model as omodel
+
+    B = X.shape[0]
+    w = np.asarray(w, dtype=np.float64)
+    out = []
+    for b, u, val in flips:
+        own = {"on": A_i[b:b + 1] > 0}
+        alt = {"on": own["on"].copy()}
+        alt["on"][0, u] = val
+        g0 = omodel.mlp_worker_grads(w, X[b][None, None], y[b][None, None], H, C, decisions=own)[0][0]
+        g1 = omodel.mlp_worker_grads(w, X[b][None, None], y[b][None, None], H, C, decisions=alt)[0][0]
+        out.append((u, (g1 - g0) / B))
+    return out
+
+
+def mlp_best_flip(a, o, deltas, d, H, C, limit=10):
+    """o' = o plus, unit by unit, the subset of that unit's flip deltas that
+    best matches a on the unit's column of dW1 and its b1 entry (where a flip
+    acts; its effect elsewhere is of the order of the pre-activation, i.e.
+    rounding).  Returns (largest per-block relative error over dW1, db1, dW2,
+    db2, o')."""
+    a = np.asarray(a, dtype=np.float64)
+    ref = np.asarray(o, dtype=np.float64).copy()
+    by_unit = {}
+    for u, dl in deltas:
+        by_unit.setdefault(u, []).append(dl)
+    for u, ds in by_unit.items():
+        assert len(ds) <= limit, (u, len(ds))
+        idx = np.r_[np.arange(u, d * H, H), d * H + u]
+        best, pick = np.inf, None
+        for m in range(1 << len(ds)):
+            cand = ref[idx] + sum((dl[idx] for i, dl in enumerate(ds) if m >> i & 1), np.zeros(idx.size))
+            err = float(np.max(np.abs(a[idx] - cand)))
+            if err < best:
+                best, pick = err, m
+        for i, dl in enumerate(ds):
+            if pick >> i & 1:
+                ref += dl
+    bounds = np.cumsum([0, d * H, H, H * C, C])
+    err = max(float(np.max(np.abs(a[lo:hi] - ref[lo:hi]))) / max(float(np.max(np.abs(ref[lo:hi]))), 1e-30)
+              for lo, hi in zip(bounds[:-1], bounds[1:]))
+    return err, ref
 
 
 def masked_rel_err(a, o, mask) -> float:

@@ -209,6 +209,38 @@ def test_cnn_finite_differences():
             assert G[0, p] == pytest.approx(fd, rel=1e-4, abs=tol), (lo, p, h)
 
 
+def test_mlp_fixed_decisions_match_finite_differences():
+    # With the ReLUs fixed (some flipped from the network's own), the loss is
+    # smooth in w and the oracle returns its gradient; its own decisions,
+    # passed in, change nothing; a flip moves its unit's W1 column and b1.
+    rng = np.random.default_rng(67)
+    B, d, H, C = 3, 12, 9, 4
+    X = rng.normal(size=(1, B, d))
+    y = rng.integers(0, C, size=(1, B))
+    w = rng.normal(size=d * H + H + H * C + C) * 0.4
+    G0, L0, A = model.mlp_worker_grads(w, X, y, H, C, return_preact=True)
+    own = {"on": A[0] > 0}
+    G1, L1 = model.mlp_worker_grads(w, X, y, H, C, decisions=own)
+    np.testing.assert_array_equal(G1, G0)
+    assert L1[0] == L0[0]
+    flip = {"on": own["on"].copy()}
+    flip["on"][1, 4] = ~flip["on"][1, 4]
+    flip["on"][2, 7] = ~flip["on"][2, 7]
+    G, _ = model.mlp_worker_grads(w, X, y, H, C, decisions=flip)
+    assert not np.array_equal(G[0, 4:d * H:H], G0[0, 4:d * H:H])
+    assert G[0, d * H + 7] != G0[0, d * H + 7]
+
+    def loss_at(v):
+        return model.mlp_worker_grads(v, X, y, H, C, decisions=flip)[1][0]
+
+    h = 1e-6
+    for p in range(w.size):
+        e = np.zeros_like(w)
+        e[p] = h
+        fd = (loss_at(w + e) - loss_at(w - e)) / (2 * h)
+        assert G[0, p] == pytest.approx(fd, rel=1e-5, abs=1e-9), p
+
+
 def test_cnn_fixed_decisions_match_finite_differences():
     # With every pooling choice and ReLU fixed (some of them flipped from the
     # network's own), the loss is a smooth function of w whose gradient the
