@@ -129,12 +129,6 @@ def mlp_best_flip(a, o, deltas, d, H, C, limit=10):
     return err, ref
 
 
-def masked_rel_err(a, o, mask) -> float:
-    a = np.asarray(a, dtype=np.float64)[mask]
-    o = np.asarray(o, dtype=np.float64)[mask]
-    return rel_err(a, o)
-
-
 def cnn_blocks(H, C):
     """[start, end) of the CNN's parameter blocks in G: Wf1, bf1, Wf2, bf2,
     Wc1, bc1, Wc2, bc2."""
