@@ -641,8 +641,8 @@ __global__ __launch_bounds__(256, 2) void k_cnn_conv1_wgrad(CnnArgs a) {
         const float g0 = gr0[px], g1 = gr1[px];
         const int c0 = cr0[px], c1 = cr1[px];
         const float x0 = xr0[2 * px], x1 = xr1[2 * px];
-        const float av0 = (c0 == g) & aval[0] ? g0 : 0.f;
-        const float av1 = (c1 == g) & aval[1] ? g1 : 0.f;
+        const float av0 = ((c0 == g) & aval[0]) ? g0 : 0.f;
+        const float av1 = ((c1 == g) & aval[1]) ? g1 : 0.f;
         const float bv0 = bx[0] ? x0 : bconst[0];
         const float bv1 = bx[1] ? x1 : bconst[1];
         acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av0, bv0, acc[0][0], 0, 0, 0);
