@@ -81,8 +81,10 @@ struct MlpArgs {
   int64_t ldG;           // row stride of G (0: P)
   float* loss;           // [n]
   // workspace
-  float* Hh;             // [n*B][H] hidden activations
+  float* Hh;             // [n*B][H] hidden activations (with ksplit 2: the first
+                         // K half's pre-activation sums, dA the second's)
   float* dA;             // [n*B][H] gradient w.r.t. pre-activations
+  int ksplit;            // set by launch_mlp_grads
   float* Gp;             // [n*slabs][H + H*C + C] head slab partials
   float* lossp;          // [n*slabs]
   int32_t* err;

@@ -152,8 +152,14 @@ __global__ __launch_bounds__(256) void k_mlp_hidden_mfma(MlpArgs a) {
   }
   mfma_f32x4 acc[WT][WT];
   mfma_zero<WT>(acc);
-  mfma_gemm_rows_w<WT>(L, xs, xrow, d, ws, H, n0, acc);
+  // with ksplit 2, block z takes one half of K (a multiple of 16) and leaves
+  // its raw sums in Hh (z = 0) or dA (z = 1); the head adds them, b1 and the
+  // ReLU (two addends: the same sum in either order)
+  const int kh = a.ksplit == 2 ? (d / 2 + MBK - 1) / MBK * MBK : d;
+  const int kbeg = static_cast<int>(blockIdx.z) * kh;
+  mfma_gemm_rows_w<WT>(L, xs, xrow, d, ws, H, n0, acc, kbeg, min(d, kbeg + kh));
   const float* b1 = a.w + (int64_t)d * H;
+  float* out = blockIdx.z == 0 ? a.Hh : a.dA;
 #pragma unroll
   for (int nt = 0; nt < WT; ++nt) {
     const int h = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
@@ -164,7 +170,7 @@ __global__ __launch_bounds__(256) void k_mlp_hidden_mfma(MlpArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t m = m0 + wm * 16 * WT + mt * 16 + 4 * (lane >> 4) + r;
-        if (m < Mrows) a.Hh[m * H + h] = fmaxf(acc[mt][nt][r] + bias, 0.f);
+        if (m < Mrows) out[m * H + h] = a.ksplit == 2 ? acc[mt][nt][r] : fmaxf(acc[mt][nt][r] + bias, 0.f);
       }
   }
 }
@@ -225,11 +231,12 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
   const float* W2 = a.w + (int64_t)d * H + H;
   const float* bias2 = W2 + (int64_t)H * C;
   const __amdgpu_buffer_rsrc_t w2s = make_rsrc(W2, static_cast<uint32_t>((int64_t)H * C * 4));
-  float wr[M][CP], gw2[M][CP], gb1[M];
+  float wr[M][CP], gw2[M][CP], gb1[M], b1v[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     const int j = tid + m * T;
     gb1[m] = 0.f;
+    b1v[m] = j < H ? a.w[(int64_t)d * H + j] : 0.f;
 #pragma unroll
     for (int c = 0; c < CP; ++c) {
       wr[m][c] = buf_f32(w2s, c < C ? static_cast<uint32_t>((j * C + c) * 4) : kOutOfRange);
@@ -245,10 +252,18 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const bool ok = cb + r < nrows;
-      const __amdgpu_buffer_rsrc_t hs =
-          make_rsrc(a.Hh + (hrow0 + b0 + (ok ? cb + r : 0)) * H, ok ? static_cast<uint32_t>(H * 4) : 0u);
+      const int64_t hoff = (hrow0 + b0 + (ok ? cb + r : 0)) * H;
+      const __amdgpu_buffer_rsrc_t hs = make_rsrc(a.Hh + hoff, ok ? static_cast<uint32_t>(H * 4) : 0u);
 #pragma unroll
       for (int m = 0; m < M; ++m) x[r][m] = buf_f32(hs, static_cast<uint32_t>((tid + m * T) * 4));
+      if (a.ksplit == 2) {
+        // the two K halves' sums (this row's dA entries are written later,
+        // by this same thread), the bias and the ReLU
+        const __amdgpu_buffer_rsrc_t h2 = make_rsrc(a.dA + hoff, ok ? static_cast<uint32_t>(H * 4) : 0u);
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+          x[r][m] = fmaxf(x[r][m] + buf_f32(h2, static_cast<uint32_t>((tid + m * T) * 4)) + b1v[m], 0.f);
+      }
     }
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -444,16 +459,22 @@ MlpPlan mlp_plan(int n, int B, int d, int H, int C) {
   return p;
 }
 
-hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& a, hipStream_t s) {
+hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& args, hipStream_t s) {
   if (!p.ok) return hipErrorNotSupported;
+  MlpArgs a = args;
+  a.ksplit = 1;
   const int64_t Mrows = (int64_t)a.n * a.B;
   const bool big = a.d % 4 == 0 && a.H % 4 == 0 && a.B <= 1024;
-  if (big && (int64_t)((a.H + 127) / 128) * ((Mrows + 127) / 128) >= kMfmaBigTiles)
+  const int64_t small_tiles = (int64_t)((a.H + 63) / 64) * ((Mrows + 63) / 64);
+  if (big && (int64_t)((a.H + 127) / 128) * ((Mrows + 127) / 128) >= kMfmaBigTiles) {
     hipLaunchKernelGGL(k_mlp_hidden_mfma<4>, dim3((a.H + 127) / 128, static_cast<unsigned>((Mrows + 127) / 128)),
                        dim3(256), 0, s, a);
-  else if (big)
-    hipLaunchKernelGGL(k_mlp_hidden_mfma<2>, dim3((a.H + 63) / 64, static_cast<unsigned>((Mrows + 63) / 64)),
-                       dim3(256), 0, s, a);
+  } else if (big) {
+    // too few 64 x 64 tiles for two blocks per CU: split K in two halves
+    if (small_tiles < kMfmaBigTiles && a.d >= 2 * MBK) a.ksplit = 2;
+    hipLaunchKernelGGL(k_mlp_hidden_mfma<2>,
+                       dim3((a.H + 63) / 64, static_cast<unsigned>((Mrows + 63) / 64), a.ksplit), dim3(256), 0, s, a);
+  }
   else
     hipLaunchKernelGGL(k_mlp_hidden, dim3((a.H + TN - 1) / TN, static_cast<unsigned>((Mrows + TM - 1) / TM)),
                        dim3(256), 0, s, a);

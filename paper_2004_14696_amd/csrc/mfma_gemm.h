@@ -68,23 +68,26 @@ __device__ __forceinline__ void mfma_slice(const MfmaLds<WT>& L, int cbuf, int w
 template <int WT>
 constexpr int mfma_pieces() { return 32 * WT / 64; }
 
-// acc += X[row(m0 + r)][k] W[k][n0 + c] over k < K, for the block's tile.
-// xrow[s] is the dataset row of tile row (tid + 256 s) / 4, or -1 for rows
-// past the matrix; W is K x N row-major (N % 4 == 0, K % 4 == 0).
+// acc += X[row(m0 + r)][k] W[k][n0 + c] over kbeg <= k < kend (default: all
+// K), for the block's tile.  xrow[s] is the dataset row of tile row
+// (tid + 256 s) / 4, or -1 for rows past the matrix; X rows have K floats;
+// W is K x N row-major (N % 4 == 0, K % 4 == 0, kbeg % 4 == 0).
 template <int WT>
 __device__ __forceinline__ void mfma_gemm_rows_w(MfmaLds<WT>& L, __amdgpu_buffer_rsrc_t xs,
                                                  const int64_t (&xrow)[mfma_pieces<WT>()], int K,
-                                                 __amdgpu_buffer_rsrc_t ws, int N, int n0, mfma_f32x4 (&acc)[WT][WT]) {
+                                                 __amdgpu_buffer_rsrc_t ws, int N, int n0, mfma_f32x4 (&acc)[WT][WT],
+                                                 int kbeg = 0, int kend = -1) {
+  if (kend < 0) kend = K;
   constexpr int NP = mfma_pieces<WT>(), BQ = 8 * WT;   // B pieces per K row
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
   auto load = [&](int k0, float4 (&ra)[NP], float4 (&rb)[NP]) {
 #pragma unroll
     for (int s2 = 0; s2 < NP; ++s2) {
       const int q = tid + s2 * 256;
-      const int k = k0 + 4 * (q % 4);
-      ra[s2] = buf_f32x4(xs, xrow[s2] >= 0 && k < K ? static_cast<uint32_t>((xrow[s2] * K + k) * 4) : kOutOfRange);
-      const int kb = k0 + q / BQ, nb = n0 + 4 * (q % BQ);
-      rb[s2] = buf_f32x4(ws, kb < K && nb < N ? static_cast<uint32_t>(((int64_t)kb * N + nb) * 4) : kOutOfRange);
+      const int k = kbeg + k0 + 4 * (q % 4);
+      ra[s2] = buf_f32x4(xs, xrow[s2] >= 0 && k < kend ? static_cast<uint32_t>((xrow[s2] * K + k) * 4) : kOutOfRange);
+      const int kb = kbeg + k0 + q / BQ, nb = n0 + 4 * (q % BQ);
+      rb[s2] = buf_f32x4(ws, kb < kend && nb < N ? static_cast<uint32_t>(((int64_t)kb * N + nb) * 4) : kOutOfRange);
     }
   };
   auto store = [&](int buf, const float4 (&ra)[NP], const float4 (&rb)[NP]) {
@@ -103,7 +106,7 @@ __device__ __forceinline__ void mfma_gemm_rows_w(MfmaLds<WT>& L, __amdgpu_buffer
   load(0, ra, rb);
   store(0, ra, rb);
   __syncthreads();
-  const int nk = (K + MBK - 1) / MBK;
+  const int nk = (kend - kbeg + MBK - 1) / MBK;
   for (int kt = 0; kt < nk; ++kt) {
     const int cbuf = kt & 1;
     if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
