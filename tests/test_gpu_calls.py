@@ -227,7 +227,7 @@ def test_worker_grads_cnn_workload_shape_sampled_workers():
         assert lg[i] == pytest.approx(lo[0], rel=RTOL)
 
 
-def test_worker_grads_cnn_rejects_other_image_sizes_and_reports_bad_rows():
+def test_worker_grads_cnn_rejects_other_image_sizes_and_reports_bad_rows_and_labels():
     with pytest.raises(pb.DBWError) as e:
         _ctx(2, 4, 785, 10, model="cnn", H=16)
     assert e.value.status == pb.DBW_EINVAL
@@ -242,6 +242,14 @@ def test_worker_grads_cnn_rejects_other_image_sizes_and_reports_bad_rows():
     with pytest.raises(pb.DBWError) as e:
         ctx.sync()
     assert e.value.status == pb.DBW_ERANGE
+    ctx.sync()                                      # the flag is cleared
+    ys = np.zeros(S, np.int32)
+    ys[7] = C                                       # a label outside [0, C) on a used row
+    idx[1, 2] = 7
+    ctx.worker_grads(to_dev(torch, w), to_dev(torch, Xs[0]), to_dev(torch, ys), rows=to_dev(torch, idx))
+    with pytest.raises(pb.DBWError) as e:
+        ctx.sync()
+    assert e.value.status == pb.DBW_EINVAL          # bad data, not a bad index
 
 
 # -- aggregation --------------------------------------------------------------------
