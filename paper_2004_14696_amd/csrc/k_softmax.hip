@@ -242,12 +242,14 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
 // features, which sit on lane % 16) are computed on the vector ALUs: each
 // lane dots its 4U features of a row with W (staged once per block in LDS,
 // in lane order), a 16-lane DPP reduction sums the row group, and the eight
-// waves' partials meet in LDS.  Every wave then runs the softmax of the
-// chunk itself, lane (m, g) producing residual r[row g + 4e][class m] --
-// the B operand of the same MFMAs.  One block barrier per chunk.
+// waves' partials meet in LDS.  Wave w then runs the softmax of row w of the
+// chunk (lane m = class) and the residuals meet in LDS again, so that lane
+// (m, g) reads r[row g + 4e][class m] -- the B operand of the same MFMAs.
+// Two block barriers per chunk.
 constexpr int MF_WAVES = 8;
 constexpr int MF_T = MF_WAVES * WAVE;
 constexpr int MF_ROWS = 8;
+static_assert(MF_ROWS == MF_WAVES, "the softmax of a chunk gives one row to each wave");
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
@@ -290,6 +292,8 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
   constexpr int WS = MF_WAVES * 16 * SL;
   __shared__ __attribute__((aligned(16))) float Ws[WS];
   __shared__ float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
+  __shared__ float rres[2][MF_ROWS][16];          // residuals of the chunk
+  __shared__ float sloss[MF_WAVES];
   __shared__ int sh_row[FUSED_MAX_ROWS];
   __shared__ int sh_lab[FUSED_MAX_ROWS];
 
@@ -469,51 +473,28 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
       }
     }
   };
-  // After the barrier: the softmax of chunk cb's rows g, g + 4 (lane m =
-  // class) from the eight waves' partials; residuals into rv, cross entropy
-  // into the label's lane.
+  // After the barrier: the softmax of chunk cb's row w (lane m = class) from
+  // the eight waves' partials, residuals into rres, cross entropy into the
+  // label's lane; after a second barrier every lane takes its rows' residuals
+  // into rv.
   auto softmax = [&](int cb, int buf) {
-    float zt[2], mx[2], ex[2], se[2];
+    // wave w: row w of the chunk, lane m = class (the four row groups repeat it)
+    const int r = cb + w;
+    const bool row_ok = r < nrows;
+    float zt = 0.f;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      zt[e] = 0.f;
+    for (int v = 0; v < MF_WAVES; ++v) zt += zb[buf][v][w][m];
+    float mx = row16_max(cls_ok ? zt : -INFINITY);
+    const float ex = cls_ok ? __expf(zt - mx) : 0.f;
+    const float se = row16_sum(ex);
+    const int lab = sh_lab[row_ok ? r : 0];
+    const bool hit = row_ok && m == lab;
+    const float p = ex * __builtin_amdgcn_rcpf(se);
+    if (g == 0) rres[buf][w][m] = row_ok && cls_ok ? (p - (hit ? 1.f : 0.f)) * invB : 0.f;
+    if (g == 0) loss_acc += hit ? __logf(se) - (zt - mx) : 0.f;
+    __syncthreads();
 #pragma unroll
-      for (int v = 0; v < MF_WAVES; ++v) zt[e] += zb[buf][v][g + 4 * e][m];
-      mx[e] = cls_ok ? zt[e] : -INFINITY;
-    }
-#pragma unroll
-    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0xB1>(mx[e]));
-#pragma unroll
-    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x4E>(mx[e]));
-#pragma unroll
-    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x141>(mx[e]));
-#pragma unroll
-    for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], dpp<0x140>(mx[e]));
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      ex[e] = cls_ok ? __expf(zt[e] - mx[e]) : 0.f;
-      se[e] = ex[e];
-    }
-#pragma unroll
-    for (int e = 0; e < 2; ++e) se[e] += dpp<0xB1>(se[e]);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) se[e] += dpp<0x4E>(se[e]);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) se[e] += dpp<0x141>(se[e]);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) se[e] += dpp<0x140>(se[e]);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int r = cb + g + 4 * e;
-      const bool row_ok = r < nrows;
-      const int lab = sh_lab[row_ok ? r : 0];
-      const bool hit = row_ok && m == lab;
-      // se >= 1 (the largest class contributes exp(0))
-      const float p = ex[e] * __builtin_amdgcn_rcpf(se[e]);
-      rv[e] = row_ok && cls_ok ? (p - (hit ? 1.f : 0.f)) * invB : 0.f;
-      // CE = log(sum_c e^{z_c - zmax}) - (z_y - zmax), in the label's lane
-      loss_acc += hit ? __logf(se[e]) - (zt[e] - mx[e]) : 0.f;
-    }
+    for (int e = 0; e < 2; ++e) rv[e] = rres[buf][g + 4 * e][m];
   };
   // One chunk: logits of chunk cb (rows in A) while chunk cb + 8 streams
   // into B, the block-wide softmax, then G += X^T R on the matrix cores.
@@ -588,14 +569,18 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
     float4* o4 = reinterpret_cast<float4*>(a.G + (int64_t)i * P);
     for (int k = tid; k < static_cast<int>(P / 4); k += MF_T) o4[k] = s4[k];
   }
-  if (w == 0) {
-    // the loss of a row sits in its label's lane of its row group
+  {
+    // the loss of row w of each chunk sits in its label's lane of wave w
     float l = loss_acc;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
-    if (lane == 0) {
-      if (slabs == 1) a.loss[i] = l * invB;
-      else a.lossp[(int64_t)i * slabs + q] = l;
+    if (lane == 0) sloss[w] = l;
+    __syncthreads();
+    if (tid == 0) {
+      float t = 0.f;
+      for (int v = 0; v < MF_WAVES; ++v) t += sloss[v];
+      if (slabs == 1) a.loss[i] = t * invB;
+      else a.lossp[(int64_t)i * slabs + q] = t;
     }
   }
 }
