@@ -1,6 +1,6 @@
 """Benchmark of the DBW hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C3] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C5] [--no-cpu-baseline]
 
 One step = one full DBW iteration (dbw_step): host time estimate, choice of
 k, all n worker minibatch gradients, fastest-k aggregation, statistics, SGD
@@ -9,9 +9,12 @@ region: the synthetic dataset, the per-iteration minibatch row indices and the
 parameters; the per-iteration round-trip ticks are host arrays, as the
 interface defines them.  Prints one JSON line.
 
-Default workload: softmax regression with 64 workers x 256 rows, 3072
-features (32x32x3-shaped) and 10 classes -- the bandwidth-bound workload the
-metric's %-of-peak-HBM figure refers to.
+Default workload: softmax regression with 256 workers x 512 rows, 3072
+features (32x32x3-shaped) and 100 classes, the largest of the five workloads
+(fp32 matrix-core bound).  The same line carries, under "hbm_roofline", the
+bandwidth-bound workload (64 workers x 256 rows, 3072 features, 10 classes)
+that the metric's %-of-peak-HBM figure refers to, and under "ps_kernels" the
+aggregation and statistics calls at fixed k = n and ceil(n/2).
 """
 from __future__ import annotations
 
@@ -31,6 +34,7 @@ METRIC = "worker-gradient samples/sec per DBW iteration (1 MI355X); % peak HBM G
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
 FUSED_MAX_CLASSES = 16         # the single-pass softmax kernel covers C <= 16
+FLUSH_BYTES = 1 << 30          # touched between launches for the cold figures (MALL is 256 MB)
 
 
 TRAFFIC_FILE = {
@@ -46,19 +50,17 @@ def measured_traffic(cfg):
     None when there is none for this workload or a kernel source it covers
     changed since it was taken."""
     import hashlib
-    import os
     path = TRAFFIC_FILE.get(cfg.name)
-    root = os.path.dirname(os.path.abspath(__file__))
-    if not path or not os.path.exists(os.path.join(root, path)):
+    if not path or not os.path.exists(os.path.join(ROOT, path)):
         return None
     rec = None
-    for line in open(os.path.join(root, path)):
+    for line in open(os.path.join(ROOT, path)):
         if line.startswith("machine-readable:"):
             rec = json.loads(line.split(":", 1)[1])
     if rec is None:
         return None
     for src, digest in rec["kernel_sources_sha256"].items():
-        with open(os.path.join(root, src), "rb") as f:
+        with open(os.path.join(ROOT, src), "rb") as f:
             if hashlib.sha256(f.read()).hexdigest() != digest:
                 return None
     return rec["traffic_bytes_per_launch"]
@@ -100,6 +102,17 @@ def roofline_bound(cfg) -> str:
     return "mfma"
 
 
+def grads_kernels(cfg) -> str:
+    """The kernels one worker-gradient launch runs (names as in the traces)."""
+    if cfg.model == "softmax":
+        if cfg.C <= FUSED_MAX_CLASSES:
+            return "k_softmax_mfma + k_slab_reduce_tiles"
+        return "k_logits_mfma + k_rows_softmax + k_grads_mfma"
+    if cfg.model == "mlp":
+        return "k_mlp_hidden_mfma + k_mlp_head + k_mlp_dw1_mfma + k_mlp_tail"
+    return "k_cnn_* + MLP kernels on the 800 features"
+
+
 def step_bytes(cfg, P: int, k: int, gathered: bool) -> int:
     """Algorithmic bytes of one iteration: gradient launch, the k received
     gradient rows read once, parameters read and written, mean gradient
@@ -107,40 +120,251 @@ def step_bytes(cfg, P: int, k: int, gathered: bool) -> int:
     return grads_bytes(cfg, P, gathered) + 4 * (k * P + 3 * P)
 
 
-def cpu_baseline(cfg, iters_cap: int, budget_s: float):
-    """The oracle timed on this host on the first iterations of the same
-    workload (bounded sample)."""
+def workload_text(cfg) -> str:
+    if cfg.model == "softmax":
+        return (f"{cfg.name}: softmax regression, n={cfg.n} workers x B={cfg.B} rows, d={cfg.d}, C={cfg.C}, "
+                f"minibatches gathered by index from a resident {cfg.S}x{cfg.d} dataset")
+    if cfg.model == "mlp":
+        return f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows"
+    return (f"{cfg.name}: CNN 28x28 conv5x5(20)-pool-conv5x5(50)-pool-FC{cfg.H}-FC{cfg.C}, "
+            f"n={cfg.n} workers x B={cfg.B} images gathered from a resident {cfg.S}-image dataset")
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, timed on this host
+def cpu_baseline(cfg, budget_s: float, budget_1core_s: float):
+    """The float64 oracle on a bounded sample of the same workload: one
+    untimed warm-up iteration (first touch of its buffers), then iterations
+    until the budget is spent.  The time estimate (Eq. quadratic_opt) is
+    solved outside the timed region and handed to the step, as the GPU
+    figure excludes it too (the library solves it on a host thread that the
+    device work hides).  BLAS threads are pinned to this process's cores;
+    a second sample runs on one core."""
+    from threadpoolctl import threadpool_info, threadpool_limits
     from dbw_inputs import gather, init_params
     from dbw_inputs import generate as gen
     from oracle import dbw as odbw
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+
+    cores = len(os.sched_getaffinity(0))
     X, y = gen.dataset(cfg)
     orc = odbw.DBWOracle(cfg, init_params(cfg))
-    done, spent = 0, 0.0
-    while done < iters_cap and spent < budget_s:
-        idx = gen.batch_indices(cfg, done)
+    state = {"t": 0}
+
+    def one(timed: bool) -> float:
+        t = state["t"]
+        idx = gen.batch_indices(cfg, t)
         Xt, yt = gather(X, y, idx)
-        ticks = gen.round_trip_ticks(cfg, done)
+        ticks = gen.round_trip_ticks(cfg, t)
+        T_hat = orc.time_estimate()             # untimed, like the GPU figure
         t0 = time.perf_counter()
-        orc.step(Xt, yt, ticks)
-        spent += time.perf_counter() - t0
-        done += 1
-    return {"value": cfg.n * cfg.B * done / spent, "unit": "samples/s", "cores": int(threads),
+        orc.step(Xt, yt, ticks, T_hat=T_hat)
+        state["t"] = t + 1
+        return time.perf_counter() - t0
+
+    def blas_threads():
+        return max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+
+    with threadpool_limits(limits=cores, user_api="blas"):
+        used = blas_threads()
+        one(False)                              # warm-up: first touch of the oracle's buffers
+        first = state["t"]
+        spent = 0.0
+        while spent < budget_s or state["t"] == first:
+            spent += one(True)
+        done = state["t"] - first
+    with threadpool_limits(limits=1, user_api="blas"):
+        used1 = blas_threads()
+        first1 = state["t"]
+        spent1 = 0.0
+        while spent1 < budget_1core_s or state["t"] == first1:
+            spent1 += one(True)
+        done1 = state["t"] - first1
+    return {"value": cfg.n * cfg.B * done / spent, "unit": "samples/s", "cores": int(used),
             "kind": "oracle",
-            "sample": f"first {done} iterations of the same workload, float64 numpy oracle "
-                      f"(minibatch gather untimed), {spent:.1f} s"}
+            "sample": f"iterations {first}..{first + done - 1} of {cfg.name} (iteration 0 untimed warm-up), "
+                      f"float64 numpy oracle, time estimate solved outside the timed region, minibatch "
+                      f"gather untimed, BLAS threads pinned to {used} with threadpoolctl, {spent:.1f} s",
+            "value_1core": cfg.n * cfg.B * done1 / spent1,
+            "sample_1core": f"the next iterations {first1}..{first1 + done1 - 1}, BLAS threads limited to "
+                            f"{used1}, {spent1:.1f} s"}
+
+
+# ---------------------------------------------------------------------------
+# GPU measurements
+class Workload:
+    """Resident inputs and a context of one workload on the GPU."""
+
+    def __init__(self, cfg, dev, n_iters: int):
+        import torch
+        import paper_2004_14696_amd as dbw
+        from dbw_inputs import init_params
+        from dbw_inputs import generate as gen
+        self.cfg = cfg
+        X, y = gen.dataset(cfg)
+        self.Xd = torch.from_numpy(np.array(X)).to(dev)
+        self.yd = torch.from_numpy(np.array(y)).to(dev)
+        self.rows = [torch.from_numpy(gen.batch_indices(cfg, t)).to(dev) for t in range(n_iters)]
+        self.ticks = [gen.round_trip_ticks(cfg, t) for t in range(n_iters)]
+        self.w = torch.from_numpy(init_params(cfg)).to(dev)
+        self.ctx = dbw.Context(dbw.config_from(cfg, S=cfg.S))
+        self.P = self.ctx.P
+        self.dev = dev
+
+    def close(self):
+        self.ctx.close()
+
+
+def time_steps(wl, warmup: int, steps: int, timing_pass: bool):
+    """Whole-job step timing (wall clock, host estimate included), then a
+    pass with per-launch-group events for the PS share."""
+    import torch
+    import paper_2004_14696_amd as dbw
+    ctx = wl.ctx
+    for t in range(warmup):
+        ctx.step(wl.w, wl.Xd, wl.yd, wl.ticks[t], rows=wl.rows[t], wait=False)
+    ctx.sync()
+    # timed region: host timers only (no device events in the launch stream)
+    ctx.profile(2)
+    ctx.profile_reset()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(ctx.stream)
+    t1 = warmup + steps
+    for t in range(warmup, t1):
+        ctx.step(wl.w, wl.Xd, wl.yd, wl.ticks[t], rows=wl.rows[t], wait=False)
+    ev1.record(ctx.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ctx.sync()
+    gpu_ms = ev0.elapsed_time(ev1)
+    host = {g: ctx.kernel_time(getattr(dbw.binding, "DBW_KT_" + g))
+            for g in ("HOST_ESTIMATE", "HOST_STEP", "HOST_WAIT", "HOST_QUEUE")}
+    agg_ms = agg_n = choose_ms = choose_n = 0
+    if timing_pass:
+        ctx.profile(1)
+        ctx.profile_reset()
+        for t in range(t1, t1 + steps):
+            ctx.step(wl.w, wl.Xd, wl.yd, wl.ticks[t], rows=wl.rows[t], wait=False)
+        ctx.sync()
+        agg_ms, agg_n = ctx.kernel_time(dbw.binding.DBW_KT_AGGREGATE)
+        choose_ms, choose_n = ctx.kernel_time(dbw.binding.DBW_KT_CHOOSE)
+    ctx.profile(False)
+    st = ctx.export_state()
+    return {"wall_ms": wall * 1e3 / steps, "gpu_ms": gpu_ms / steps,
+            "agg_ms": agg_ms / steps if agg_n else None, "choose_ms": choose_ms / steps if choose_n else None,
+            "host": {k: v[0] / max(v[1], 1) for k, v in host.items()}, "k_last": st["k_prev"]}
+
+
+def time_grads(wl, first: int, steps: int):
+    """The worker-gradient call (dbw_worker_grads) alone: warm = back to back
+    between two events on the context stream; cold = each launch after a
+    1 GiB buffer was read and written (untimed), which evicts the 256 MB
+    MALL and the L2s, with events around the launch only."""
+    import torch
+    ctx, cfg = wl.ctx, wl.cfg
+    G = torch.empty((cfg.n, wl.P), dtype=torch.float32, device=wl.dev)
+    Lb = torch.empty(cfg.n, dtype=torch.float32, device=wl.dev)
+    ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first], G=G, loss=Lb)
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(ctx.stream)
+    for t in range(steps):
+        ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first + t], G=G, loss=Lb)
+    g1.record(ctx.stream)
+    torch.cuda.synchronize()
+    warm_ms = g0.elapsed_time(g1) / steps
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=wl.dev)
+    cold = 0.0
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for t in range(steps):
+        flush.add_(1.0)
+        evs[t][0].record(ctx.stream)
+        ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first + t], G=G, loss=Lb)
+        evs[t][1].record(ctx.stream)
+    torch.cuda.synchronize()
+    cold = sum(a.elapsed_time(b) for a, b in evs) / steps
+    del flush
+    ctx.sync()
+    return warm_ms, cold, G, Lb
+
+
+def roofline_block(cfg, P: int, warm_ms: float, cold_ms: float, launches: int) -> dict:
+    gb = grads_bytes(cfg, P, True)
+    bound = roofline_bound(cfg)
+    if bound == "hbm":
+        work, peak, unit = gb / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        work, peak, unit = grads_flops(cfg) / 1e12, MFMA_F32_PEAK_TFLOPS, "TFLOP/s"
+    achieved = work / (warm_ms / 1e3)
+    achieved_cold = work / (cold_ms / 1e3)
+    return {
+        "kernel": f"worker-gradient launch dbw_worker_grads ({grads_kernels(cfg)}); every G row written",
+        "bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+        "traffic": measured_traffic(cfg), "bytes_per_launch": gb, "flops_per_launch": grads_flops(cfg),
+        "avg_launch_ms": warm_ms, "launches": launches,
+        "cold": {"avg_launch_ms": cold_ms, "achieved": achieved_cold, "frac": achieved_cold / peak,
+                 "flush": "1 GiB device buffer read and written before each launch (untimed)"},
+    }
+
+
+def ps_fixed_k(wl, G, Lb, reps: int = 10):
+    """The aggregation call (dbw_aggregate_fastest: rank selection, then the
+    k rows streamed once into g) and the statistics call (dbw_grad_stats:
+    mask to list, the k rows streamed against g, fixed-order finish) at
+    fixed k = n and ceil(n/2) on the workload's gradient rows."""
+    import torch
+    ctx, cfg, P = wl.ctx, wl.cfg, wl.P
+    n = cfg.n
+    ticks = torch.from_numpy(np.ascontiguousarray(wl.ticks[0], dtype=np.int64)).to(wl.dev)
+    g = torch.empty(P, dtype=torch.float32, device=wl.dev)
+    mask = torch.empty(n, dtype=torch.uint8, device=wl.dev)
+    sq = torch.empty(n, dtype=torch.float32, device=wl.dev)
+    stats = torch.empty(4, dtype=torch.float64, device=wl.dev)
+    out = []
+    for k in (n, (n + 1) // 2):
+        ctx.aggregate_fastest(G, ticks, k, g=g, mask=mask)
+        ctx.grad_stats(G, mask, k, g, Lb, sqnorm=sq, stats=stats)
+        ctx.sync()
+        res = {"k": k}
+        for name, fn, nbytes in (
+                ("aggregate", lambda: ctx.aggregate_fastest(G, ticks, k, g=g, mask=mask),
+                 4 * (k * P + P) + 9 * n),
+                ("stats", lambda: ctx.grad_stats(G, mask, k, g, Lb, sqnorm=sq, stats=stats),
+                 4 * (k * P + P) + 9 * n + 32)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(ctx.stream)
+            for _ in range(reps):
+                fn()
+            e1.record(ctx.stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            gbs = nbytes / (ms / 1e3) / 1e9
+            res[name] = {"ms": ms, "bytes": nbytes, "GB/s": gbs, "hbm_frac": gbs / HBM_PEAK_GBS}
+        ctx.sync()
+        out.append(res)
+    return out
+
+
+def measure(cfg, args, dev, with_ps: bool):
+    total = args.warmup + 2 * args.steps + 1
+    wl = Workload(cfg, dev, total)
+    st = time_steps(wl, args.warmup, args.steps, timing_pass=not args.no_kernel_timing)
+    first = args.warmup + args.steps
+    warm_ms, cold_ms, G, Lb = time_grads(wl, first, args.steps)
+    res = {"step": st, "roofline": roofline_block(cfg, wl.P, warm_ms, cold_ms, args.steps), "P": wl.P}
+    if with_ps:
+        res["ps_kernels"] = ps_fixed_k(wl, G, Lb)
+    del G, Lb
+    wl.close()
+    return res
 
 
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="C3")
+    ap.add_argument("--workload", default="C5")
     ap.add_argument("--clock", choices=("fresh", "psw", "psi"), default="fresh",
                     help="virtual clock: every worker starts each iteration afresh, Push & Wait, "
                          "or Push & Interrupt")
@@ -155,8 +379,11 @@ def main(argv=None) -> int:
                          "kernel splits rows into slabs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget-1core", type=float, default=10.0)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the named workload: no bandwidth-bound companion line, no fixed-k PS calls")
     ap.add_argument("--no-kernel-timing", action="store_true",
-                    help="skip the per-launch HIP events (the roofline fields are then omitted)")
+                    help="skip the per-launch-group event pass of the steps")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for hardware-counter passes: three 256 MiB device copies (the calibration), "
                          "then five gradient launches of the workload; prints no bench line")
@@ -168,17 +395,18 @@ def main(argv=None) -> int:
 
     import torch
 
-    import paper_2004_14696_amd as dbw
-    from dbw_inputs import get, init_params
-    from dbw_inputs import generate as gen
+    from dbw_inputs import get
 
-    cfg = get(args.workload)
-    if args.clock != cfg.clock:
-        cfg = cfg.replace(clock=args.clock)
-    if args.policy == "static" and not 1 <= args.k_static <= cfg.n:
-        sys.exit(f"--policy static needs --k-static in [1, {cfg.n}]")
-    cfg = cfg.replace(policy=args.policy, k_static=args.k_static if args.policy == "static" else 0,
-                      estimator=args.estimator, g_rows=args.g_rows)
+    def configure(name):
+        cfg = get(name)
+        if args.clock != cfg.clock:
+            cfg = cfg.replace(clock=args.clock)
+        if args.policy == "static" and not 1 <= args.k_static <= cfg.n:
+            sys.exit(f"--policy static needs --k-static in [1, {cfg.n}]")
+        return cfg.replace(policy=args.policy, k_static=args.k_static if args.policy == "static" else 0,
+                           estimator=args.estimator, g_rows=args.g_rows)
+
+    cfg = configure(args.workload)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     if args.traffic_probe:
@@ -187,86 +415,23 @@ def main(argv=None) -> int:
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-    X, y = gen.dataset(cfg)
-    Xd = torch.from_numpy(np.ascontiguousarray(X)).to(dev)
-    yd = torch.from_numpy(np.ascontiguousarray(y)).to(dev)
-    timing_pass = not args.no_kernel_timing
-    total = args.warmup + args.steps * (2 if timing_pass else 1)
-    rows = [torch.from_numpy(gen.batch_indices(cfg, t)).to(dev) for t in range(total)]
-    ticks = [gen.round_trip_ticks(cfg, t) for t in range(total)]
-    w = torch.from_numpy(init_params(cfg)).to(dev)
-    ctx = dbw.Context(dbw.config_from(cfg, S=cfg.S))
-    P = ctx.P
-
-    if args.traffic_probe:
-        G = torch.empty((cfg.n, P), dtype=torch.float32, device=dev)
+        del src, dst
+        wl = Workload(cfg, dev, 5)
+        G = torch.empty((cfg.n, wl.P), dtype=torch.float32, device=dev)
         Lb = torch.empty(cfg.n, dtype=torch.float32, device=dev)
         for t in range(5):
-            ctx.worker_grads(w, Xd, yd, rows=rows[t % len(rows)], G=G, loss=Lb)
-        ctx.sync()
+            wl.ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[t], G=G, loss=Lb)
+        wl.ctx.sync()
         print(f"traffic probe: 3 copies of 256 MiB, 5 gradient launches of {cfg.name}", flush=True)
         return 0
 
-    ks = []
-    for t in range(args.warmup):
-        ks.append(ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False))
-    ctx.sync()
-    # timed region: host timers only (no device events in the launch stream)
-    ctx.profile(2)
-    ctx.profile_reset()
-    stream = ctx.stream
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    ev0.record(stream)
-    t1 = args.warmup + args.steps
-    for t in range(args.warmup, t1):
-        ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ctx.sync()
-    gpu_ms = ev0.elapsed_time(ev1)
-    host = {g: ctx.kernel_time(getattr(dbw.binding, "DBW_KT_" + g))
-            for g in ("HOST_ESTIMATE", "HOST_STEP", "HOST_WAIT", "HOST_QUEUE")}
-    # kernel-timing pass: the same loop continued with events around every
-    # launch group (their cost stays out of the timed region above)
-    grads_ms = grads_n = agg_ms = agg_n = choose_ms = choose_n = 0
-    if timing_pass:
-        ctx.profile(1)
-        ctx.profile_reset()
-        for t in range(t1, total):
-            ctx.step(w, Xd, yd, ticks[t], rows=rows[t], wait=False)
-        ctx.sync()
-        agg_ms, agg_n = ctx.kernel_time(dbw.binding.DBW_KT_AGGREGATE)
-        choose_ms, choose_n = ctx.kernel_time(dbw.binding.DBW_KT_CHOOSE)
-        ctx.profile(False)
-        # the gradient launch alone, back to back on the context stream with
-        # the step's inputs, bracketed by two events (no per-launch events)
-        G = torch.empty((cfg.n, P), dtype=torch.float32, device=dev)
-        Lb = torch.empty(cfg.n, dtype=torch.float32, device=dev)
-        ctx.worker_grads(w, Xd, yd, rows=rows[0], G=G, loss=Lb)
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        g0.record(stream)
-        for t in range(args.steps):
-            ctx.worker_grads(w, Xd, yd, rows=rows[t1 + t], G=G, loss=Lb)
-        g1.record(stream)
-        torch.cuda.synchronize()
-        grads_ms, grads_n = g0.elapsed_time(g1), args.steps
-    ctx.profile(False)
-    st = ctx.export_state()
-    k_last = st["k_prev"]
-
-    ms_per_step = wall * 1e3 / args.steps     # whole job: host estimate, launches, device work
+    extras = not args.no_extras and args.workload == "C5"
+    main_res = measure(cfg, args, dev, with_ps=extras)
+    st = main_res["step"]
+    P = main_res["P"]
+    ms_per_step = st["wall_ms"]     # whole job: host estimate, launches, device work
     value = cfg.n * cfg.B / (ms_per_step / 1e3)
-    gb = grads_bytes(cfg, P, True)
-    grads_avg_s = grads_ms / max(grads_n, 1) / 1e3 if grads_n else float("nan")
-    bound = roofline_bound(cfg)
-    if bound == "hbm":
-        achieved, peak, unit = gb / grads_avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved, peak, unit = grads_flops(cfg) / grads_avg_s / 1e12, MFMA_F32_PEAK_TFLOPS, "TFLOP/s"
-    sb = step_bytes(cfg, P, k_last, True)
+    sb = step_bytes(cfg, P, st["k_last"], True)
     out = {
         "metric": METRIC,
         "value": value,
@@ -281,45 +446,46 @@ def main(argv=None) -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"{cfg.name}: softmax regression, n={cfg.n} workers x B={cfg.B} rows, d={cfg.d}, "
-                        f"C={cfg.C}, minibatches gathered by index from a resident {cfg.S}x{cfg.d} dataset"
-            if cfg.model == "softmax" else
-            f"{cfg.name}: MLP {cfg.d}-{cfg.H}-{cfg.C}, n={cfg.n} workers x B={cfg.B} rows"
-            if cfg.model == "mlp" else
-            f"{cfg.name}: CNN 28x28 conv5x5(20)-pool-conv5x5(50)-pool-FC{cfg.H}-FC{cfg.C}, "
-            f"n={cfg.n} workers x B={cfg.B} images gathered from a resident {cfg.S}-image dataset",
+            "workload": workload_text(cfg),
             "n": cfg.n, "B": cfg.B, "d": cfg.d, "C": cfg.C, "H": cfg.H, "P": P, "clock": cfg.clock,
             "policy": cfg.policy, "k_static": cfg.k_static, "estimator": cfg.estimator, "g_rows": cfg.g_rows,
         },
-        "roofline": {
-            "kernel": "worker gradients (dbw_worker_grads)",
-            "bound": bound,
-            "achieved": achieved,
-            "peak": peak,
-            "unit": unit,
-            "frac": achieved / peak,
-            "traffic": measured_traffic(cfg),
-            "bytes_per_launch": gb,
-            "flops_per_launch": grads_flops(cfg),
-            "avg_launch_ms": grads_avg_s * 1e3,
-            "launches": grads_n,
-        },
+        "roofline": main_res["roofline"],
         "step": {
-            "gpu_ms_per_step": gpu_ms / args.steps,
-            "wall_ms_per_step": wall * 1e3 / args.steps,
+            "gpu_ms_per_step": st["gpu_ms"],
+            "wall_ms_per_step": st["wall_ms"],
             "bytes_per_step": sb,
             "hbm_frac": sb / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS,
-            "aggregate_and_stats_ms_per_step": agg_ms / args.steps if agg_n else None,
-            "choose_ms_per_step": choose_ms / args.steps if choose_n else None,
-            "host_estimate_ms_per_step": host["HOST_ESTIMATE"][0] / max(host["HOST_ESTIMATE"][1], 1),
-            "host_step_call_ms": host["HOST_STEP"][0] / max(host["HOST_STEP"][1], 1),
-            "host_wait_for_estimate_ms": host["HOST_WAIT"][0] / max(host["HOST_WAIT"][1], 1),
-            "host_queue_ms": host["HOST_QUEUE"][0] / max(host["HOST_QUEUE"][1], 1),
-            "k_last": k_last,
+            "aggregate_and_stats_ms_per_step": st["agg_ms"],
+            "choose_ms_per_step": st["choose_ms"],
+            "host_estimate_ms_per_step": st["host"]["HOST_ESTIMATE"],
+            "host_step_call_ms": st["host"]["HOST_STEP"],
+            "host_wait_for_estimate_ms": st["host"]["HOST_WAIT"],
+            "host_queue_ms": st["host"]["HOST_QUEUE"],
+            "k_last": st["k_last"],
         },
     }
+    if extras:
+        out["ps_kernels"] = {
+            "workload": cfg.name,
+            "calls": main_res["ps_kernels"],
+            "note": "whole calls by HIP events (rank selection or mask-to-list, the streaming kernel, "
+                    "and for the statistics the fixed-order finish); bytes = the k rows read once, g "
+                    "written or read, ticks/mask/loss/sqnorm",
+        }
+        c3 = configure("C3")
+        r3 = measure(c3, args, dev, with_ps=False)
+        s3 = r3["step"]
+        out["hbm_roofline"] = {
+            "workload": workload_text(c3),
+            **r3["roofline"],
+            "step_ms": s3["wall_ms"],
+            "step_samples_per_s": c3.n * c3.B / (s3["wall_ms"] / 1e3),
+            "g_rows": c3.g_rows,
+            "k_last": s3["k_last"],
+        }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, iters_cap=1000, budget_s=args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_budget, args.cpu_budget_1core)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -50,3 +50,17 @@ def test_measured_traffic_follows_kernel_source(tmp_path, monkeypatch):
 def test_more_than_one_gpu_is_refused(capsys):
     assert bench.main(["--gpus", "2"]) == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_roofline_block_warm_and_cold():
+    # C5: 1.61e11 useful flops per launch; 2 ms warm and 2.5 ms cold
+    cfg = get("C5")
+    r = bench.roofline_block(cfg, cfg.d * cfg.C, 2.0, 2.5, 20)
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s"
+    assert r["achieved"] == pytest.approx(bench.grads_flops(cfg) / 2e-3 / 1e12)
+    assert r["frac"] == pytest.approx(r["achieved"] / bench.MFMA_F32_PEAK_TFLOPS)
+    assert r["cold"]["achieved"] == pytest.approx(r["achieved"] * 2.0 / 2.5)
+    c3 = get("C3")
+    r3 = bench.roofline_block(c3, c3.d * c3.C, 0.05, 0.06, 20)
+    assert r3["bound"] == "hbm" and r3["unit"] == "GB/s"
+    assert r3["achieved"] == pytest.approx(209445120 / 0.05e-3 / 1e9)
