@@ -107,6 +107,8 @@ def grads_kernels(cfg) -> str:
     if cfg.model == "softmax":
         if cfg.C <= FUSED_MAX_CLASSES:
             return "k_softmax_mfma + k_slab_reduce_tiles"
+        if cfg.C <= 112 and cfg.C % 4 == 0 and cfg.d % 4 == 0:
+            return "k_logits_softmax_mfma + k_grads_mfma_n"
         return "k_logits_mfma + k_rows_softmax + k_grads_mfma"
     if cfg.model == "mlp":
         return "k_mlp_hidden_mfma + k_mlp_head + k_mlp_dw1_mfma + k_mlp_tail"
@@ -118,6 +120,11 @@ def step_bytes(cfg, P: int, k: int, gathered: bool) -> int:
     gradient rows read once, parameters read and written, mean gradient
     written."""
     return grads_bytes(cfg, P, gathered) + 4 * (k * P + 3 * P)
+
+
+def log(msg: str) -> None:
+    """Progress on stderr (the JSON line is the only stdout output)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def workload_text(cfg) -> str:
@@ -259,8 +266,9 @@ def time_steps(wl, warmup: int, steps: int, timing_pass: bool):
 def time_grads(wl, first: int, steps: int):
     """The worker-gradient call (dbw_worker_grads) alone: warm = back to back
     between two events on the context stream; cold = each launch after a
-    1 GiB buffer was read and written (untimed), which evicts the 256 MB
-    MALL and the L2s, with events around the launch only."""
+    1 GiB buffer was read (untimed), which evicts the 256 MB MALL and the
+    L2s without leaving dirty lines behind, with events around the launch
+    only."""
     import torch
     ctx, cfg = wl.ctx, wl.cfg
     G = torch.empty((cfg.n, wl.P), dtype=torch.float32, device=wl.dev)
@@ -277,7 +285,7 @@ def time_grads(wl, first: int, steps: int):
     cold = 0.0
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for t in range(steps):
-        flush.add_(1.0)
+        flush.sum()                   # read-only: no dirty lines left to write back
         evs[t][0].record(ctx.stream)
         ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first + t], G=G, loss=Lb)
         evs[t][1].record(ctx.stream)
@@ -303,7 +311,7 @@ def roofline_block(cfg, P: int, warm_ms: float, cold_ms: float, launches: int) -
         "traffic": measured_traffic(cfg), "bytes_per_launch": gb, "flops_per_launch": grads_flops(cfg),
         "avg_launch_ms": warm_ms, "launches": launches,
         "cold": {"avg_launch_ms": cold_ms, "achieved": achieved_cold, "frac": achieved_cold / peak,
-                 "flush": "1 GiB device buffer read and written before each launch (untimed)"},
+                 "flush": "1 GiB device buffer read before each launch (untimed)"},
     }
 
 
@@ -347,12 +355,16 @@ def ps_fixed_k(wl, G, Lb, reps: int = 10):
 
 def measure(cfg, args, dev, with_ps: bool):
     total = args.warmup + 2 * args.steps + 1
+    log(f"{cfg.name}: inputs")
     wl = Workload(cfg, dev, total)
+    log(f"{cfg.name}: {args.warmup} + {args.steps} steps")
     st = time_steps(wl, args.warmup, args.steps, timing_pass=not args.no_kernel_timing)
     first = args.warmup + args.steps
+    log(f"{cfg.name}: gradient launches, warm and cold")
     warm_ms, cold_ms, G, Lb = time_grads(wl, first, args.steps)
     res = {"step": st, "roofline": roofline_block(cfg, wl.P, warm_ms, cold_ms, args.steps), "P": wl.P}
     if with_ps:
+        log(f"{cfg.name}: aggregation and statistics at fixed k")
         res["ps_kernels"] = ps_fixed_k(wl, G, Lb)
     del G, Lb
     wl.close()
@@ -485,6 +497,7 @@ def main(argv=None) -> int:
             "k_last": s3["k_last"],
         }
     if not args.no_cpu_baseline:
+        log(f"{cfg.name}: CPU baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_budget, args.cpu_budget_1core)
     print(json.dumps(out), flush=True)
     return 0

@@ -913,6 +913,233 @@ __global__ __launch_bounds__(256) void k_grads_mfma(SoftmaxArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core path for 16 < C <= 16 NT (C % 4 == 0): the narrow-N loops of
+// mfma_gemm.h put all classes of a row in one wave, so the row softmax runs
+// in the logits kernel's registers (a 16-lane DPP row holds the row's
+// classes) and the residuals are written once; then G_i = X_i^T R_i with
+// blocks of 64 MT features x all classes.
+constexpr int NARROW_MT = 2;
+
+// Z[m][c] = (softmax(x_m W)_c - [c = y_m]) / B, ce[m] = CE of row m;
+// blockIdx.x = tile of 64 MT rows.
+template <int MT, int NT>
+__global__ __launch_bounds__(256) void k_logits_softmax_mfma(SoftmaxArgs a) {
+  using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
+  constexpr int BM = Lds::BM, BN = Lds::BN;
+  constexpr int NPA = BM / 64;                          // A: BM rows x 4 float4
+  constexpr int NPB = (4 * BN + 255) / 256;             // B: 16 k rows x BN / 4 float4
+  __shared__ Lds L;
+  __shared__ int sh_lab[BM];
+  const int tid = threadIdx.x, lane = tid & 63, wm = tid >> 6;
+  const int64_t Mrows = (int64_t)a.n * a.B;
+  const int64_t m0 = (int64_t)blockIdx.x * BM;
+  const int d = a.d, C = a.C;
+  const int64_t xrows = a.rows ? a.S : Mrows;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t ws = make_rsrc(a.W, static_cast<uint32_t>((int64_t)d * C * 4));
+  if (tid < BM) {
+    const int64_t m = m0 + tid;
+    int lab = 0;
+    if (m < Mrows) {
+      const int64_t row = sample_row(a, static_cast<int>(m / a.B), static_cast<int>(m % a.B), true);
+      lab = sample_label(a, row, true);
+    }
+    sh_lab[tid] = lab;
+  }
+  int64_t xrow[NPA];
+#pragma unroll
+  for (int s2 = 0; s2 < NPA; ++s2) {
+    const int64_t m = m0 + (tid + s2 * 256) / 4;
+    xrow[s2] = m < Mrows ? sample_row(a, static_cast<int>(m / a.B), static_cast<int>(m % a.B), false) : -1;
+  }
+  auto load = [&](int k0, float4 (&ra)[NPA], float4 (&rb)[NPB]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NPA; ++s2) {
+      const int k = k0 + 4 * ((tid + s2 * 256) % 4);
+      ra[s2] = buf_f32x4(xs, xrow[s2] >= 0 && k < d ? static_cast<uint32_t>((xrow[s2] * d + k) * 4) : kOutOfRange);
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NPB; ++s2) {
+      const int q = tid + s2 * 256;
+      const int kb = k0 + q / (BN / 4), nb = 4 * (q % (BN / 4));
+      rb[s2] = buf_f32x4(ws, q < 4 * BN && kb < d && nb < C ? static_cast<uint32_t>(((int64_t)kb * C + nb) * 4)
+                                                             : kOutOfRange);
+    }
+  };
+  auto store = [&](int buf, const float4 (&ra)[NPA], const float4 (&rb)[NPB]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NPA; ++s2) {
+      const int q = tid + s2 * 256;
+      const int r = q / 4, k = 4 * (q % 4);
+      L.A[buf][k + 0][r] = ra[s2].x;
+      L.A[buf][k + 1][r] = ra[s2].y;
+      L.A[buf][k + 2][r] = ra[s2].z;
+      L.A[buf][k + 3][r] = ra[s2].w;
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NPB; ++s2) {
+      const int q = tid + s2 * 256;
+      if (q < 4 * BN) *reinterpret_cast<float4*>(&L.B[buf][q / (BN / 4)][4 * (q % (BN / 4))]) = rb[s2];
+    }
+  };
+  mfma_f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+  mfma_pipeline_n<MT, NT, 64 * MT + 4, NPA, NPB>(L, (d + MBK - 1) / MBK, load, store, acc);
+
+  // row softmax: lane l holds rows 4 (l / 16) + r of each 16-row tile, class
+  // 16 nt + l % 16; a row's classes are the 16 lanes of one DPP row
+  const float invB = 1.0f / static_cast<float>(a.B);
+  const int cl = lane & 15;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rl = wm * 16 * MT + mt * 16 + 4 * (lane >> 4) + r;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        if (nt * 16 + cl < C) mx = fmaxf(mx, acc[mt][nt][r]);
+      mx = row16_max(mx);
+      float ex[NT];
+      float se = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        ex[nt] = nt * 16 + cl < C ? expf(acc[mt][nt][r] - mx) : 0.f;
+        se += ex[nt];
+      }
+      se = row16_sum(se);
+      const int64_t m = m0 + rl;
+      if (m < Mrows) {
+        const int lab = sh_lab[rl];
+        const float inv = 1.0f / se;
+        float* z = a.Z + m * C;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int c = nt * 16 + cl;
+          if (c < C) z[c] = (ex[nt] * inv - (c == lab ? 1.f : 0.f)) * invB;
+          if (c == lab) a.ce[m] = (logf(se) + mx) - acc[mt][nt][r];
+        }
+      }
+    }
+}
+
+// G_i[j][c] = sum_b X[row(i,b)][j] R_i[b][c] for a block of 64 MT features
+// and all classes; blockIdx.x = feature tile, y = worker.  Block (0, i) also
+// writes loss_i.
+template <int MT, int NT>
+__global__ __launch_bounds__(256) void k_grads_mfma_n(SoftmaxArgs a) {
+  using Lds = MfmaLdsN<MT, NT, 64 * MT + 16>;
+  constexpr int BM = Lds::BM, BN = Lds::BN;
+  constexpr int NPA = BM / 64;                          // A: 16 rows x BM / 4 float4
+  constexpr int NPB = (4 * BN + 255) / 256;             // B: 16 rows x BN / 4 float4
+  __shared__ Lds L;
+  __shared__ int sh_row[FUSED_MAX_ROWS];
+  __shared__ float sh[256];
+  const int tid = threadIdx.x, lane = tid & 63, wm = tid >> 6;
+  const int i = blockIdx.y;
+  const int j0 = blockIdx.x * BM;
+  const int d = a.d, C = a.C, B = a.B;
+  const int64_t P = (int64_t)d * C;
+  const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
+  const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.Z + (int64_t)i * B * C, static_cast<uint32_t>((int64_t)B * C * 4));
+  for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(sample_row(a, i, b, false));
+  __syncthreads();
+  auto load = [&](int k0, float4 (&ra)[NPA], float4 (&rb)[NPB]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NPA; ++s2) {
+      const int q = tid + s2 * 256;
+      const int b = k0 + q / (BM / 4), j = j0 + 4 * (q % (BM / 4));
+      ra[s2] = buf_f32x4(xs, b < B && j < d ? static_cast<uint32_t>(((int64_t)sh_row[b] * d + j) * 4) : kOutOfRange);
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NPB; ++s2) {
+      const int q = tid + s2 * 256;
+      const int b = k0 + q / (BN / 4), c = 4 * (q % (BN / 4));
+      rb[s2] = buf_f32x4(rs, q < 4 * BN && b < B && c < C ? static_cast<uint32_t>(((int64_t)b * C + c) * 4)
+                                                         : kOutOfRange);
+    }
+  };
+  auto store = [&](int buf, const float4 (&ra)[NPA], const float4 (&rb)[NPB]) {
+#pragma unroll
+    for (int s2 = 0; s2 < NPA; ++s2) {
+      const int q = tid + s2 * 256;
+      *reinterpret_cast<float4*>(&L.A[buf][q / (BM / 4)][4 * (q % (BM / 4))]) = ra[s2];
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NPB; ++s2) {
+      const int q = tid + s2 * 256;
+      if (q < 4 * BN) *reinterpret_cast<float4*>(&L.B[buf][q / (BN / 4)][4 * (q % (BN / 4))]) = rb[s2];
+    }
+  };
+  mfma_f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+  mfma_pipeline_n<MT, NT, 64 * MT + 16, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
+  float* Gi = a.G + (int64_t)i * P;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + wm * 16 * MT + mt * 16 + 4 * (lane >> 4) + r;
+      if (j >= d) continue;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int c = nt * 16 + (lane & 15);
+        if (c < C) Gi[(int64_t)j * C + c] = acc[mt][nt][r];
+      }
+    }
+  if (blockIdx.x == 0) {
+    // loss_i = mean CE over the worker's rows (fixed order)
+    float s = 0.f;
+    for (int b = tid; b < B; b += 256) s += a.ce[(int64_t)i * B + b];
+    sh[tid] = s;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (tid < st) sh[tid] += sh[tid + st];
+      __syncthreads();
+    }
+    if (tid == 0) a.loss[i] = sh[0] / static_cast<float>(B);
+  }
+}
+
+template <int NT>
+hipError_t launch_narrow_t(const SoftmaxArgs& a, hipStream_t s) {
+  const int64_t Mrows = (int64_t)a.n * a.B;
+  constexpr int BM = 64 * NARROW_MT;
+  hipLaunchKernelGGL((k_logits_softmax_mfma<NARROW_MT, NT>), dim3(static_cast<unsigned>((Mrows + BM - 1) / BM)),
+                     dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_grads_mfma_n<NARROW_MT, NT>), dim3(static_cast<unsigned>((a.d + BM - 1) / BM), a.n),
+                     dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// Classes per 16-wide MFMA tile for the narrow path (0: not taken).
+int narrow_tiles(int C, int d, int B) {
+  if (C <= 16 || C > 112 || C % 4 != 0 || d % 4 != 0 || B > FUSED_MAX_ROWS) return 0;
+  return (C + 15) / 16;
+}
+
+hipError_t launch_narrow(const SoftmaxArgs& a, hipStream_t s) {
+  switch (narrow_tiles(a.C, a.d, a.B)) {
+    case 2: return launch_narrow_t<2>(a, s);
+    case 3: return launch_narrow_t<3>(a, s);
+    case 4: return launch_narrow_t<4>(a, s);
+    case 5: return launch_narrow_t<5>(a, s);
+    case 6: return launch_narrow_t<6>(a, s);
+    case 7: return launch_narrow_t<7>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int CP, int M, int T>
 hipError_t launch_fused_t(const SoftmaxPlan& p, const SoftmaxArgs& a, hipStream_t s) {
   constexpr int R = 4;
@@ -1052,6 +1279,7 @@ hipError_t launch_softmax_grads(const SoftmaxPlan& p, const SoftmaxArgs& a, hipS
     }
     return hipErrorInvalidValue;
   }
+  if (narrow_tiles(a.C, a.d, a.B)) return launch_narrow(a, s);
   const int64_t Mrows = (int64_t)a.n * a.B;
   // matrix cores when float4 pieces tile the rows of X, W and R exactly
   // (and a worker's row indices fit the LDS stage)

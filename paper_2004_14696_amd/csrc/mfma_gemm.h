@@ -157,4 +157,58 @@ __device__ __forceinline__ void mfma_gemm_xt_r(MfmaLds<WT>& L, __amdgpu_buffer_r
   }
 }
 
+// ---------------------------------------------------------------------------
+// Narrow-N variant: four waves stacked along M, each owning MT x NT tiles of
+// 16 x 16, so a block covers (64 MT) x (16 NT) outputs and the whole N extent
+// lives in one wave (N up to 16 NT: e.g. 100 classes in 7 tiles instead of a
+// 128-wide tile).  A rows are AST floats apart in LDS, B rows BST.
+template <int MT, int NT, int AST>
+struct MfmaLdsN {
+  static constexpr int BM = 64 * MT, BN = 16 * NT;
+  // B rows 16 mod 64 floats apart: the four k rows of one read hit disjoint
+  // bank quarters
+  static constexpr int BST = (BN + 63) / 64 * 64 + 16;
+  float A[2][MBK][AST];
+  float B[2][MBK][BST];
+};
+
+template <int MT, int NT, int AST>
+__device__ __forceinline__ void mfma_slice_n(const MfmaLdsN<MT, NT, AST>& L, int cbuf, int wm, int lane,
+                                             mfma_f32x4 (&acc)[MT][NT]) {
+  const int i = lane & 15, kq = lane >> 4;
+#pragma unroll
+  for (int ks = 0; ks < MBK; ks += 4) {
+    float av[MT], bv[NT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) av[t] = L.A[cbuf][ks + kq][wm * 16 * MT + t * 16 + i];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) bv[t] = L.B[cbuf][ks + kq][t * 16 + i];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+  }
+}
+
+// The slice pipeline shared by the narrow-N GEMMs: load(k0, ra, rb) fetches
+// slice k0 into registers, store(buf, ra, rb) puts it into LDS buffer buf.
+// NPA / NPB float4 pieces per thread.
+template <int MT, int NT, int AST, int NPA, int NPB, class Load, class Store>
+__device__ __forceinline__ void mfma_pipeline_n(MfmaLdsN<MT, NT, AST>& L, int nk, Load load, Store store,
+                                                mfma_f32x4 (&acc)[MT][NT]) {
+  const int lane = threadIdx.x & 63, wm = threadIdx.x >> 6;
+  float4 ra[NPA], rb[NPB];
+  load(0, ra, rb);
+  store(0, ra, rb);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cbuf = kt & 1;
+    if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
+    mfma_slice_n<MT, NT, AST>(L, cbuf, wm, lane, acc);
+    if (kt + 1 < nk) store(cbuf ^ 1, ra, rb);
+    __syncthreads();
+  }
+}
+
 }  // namespace dbw

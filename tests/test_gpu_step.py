@@ -177,6 +177,8 @@ def _lockstep(cfg, iters, seed_rows=False):
                                       V_window if V_window is not None else 0.0))
         same = _compare_iteration(cfg, rec, out, k_gpu, w32, host(wd), st_before, st_after, (cfg.name, t))
         ties += not same
+        if iters >= 50:
+            print(f"lockstep {cfg.name} g_rows={cfg.g_rows}: iteration {t} k={k_gpu}", flush=True)
         if same:
             assert np.array_equal(cnt_g, np.array(orc.cnt, np.int64)), (cfg.name, t)
             assert np.array_equal(tsum_g, np.array(orc.tsum, np.int64)), (cfg.name, t)
