@@ -168,6 +168,8 @@ int64_t dbw_param_count(const dbw_config* cfg);
  * would reach 2 GiB. */
 dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out);
 void dbw_destroy(dbw_ctx* ctx);
+/* Text of the last failure on ctx; with ctx NULL, of the last failed
+ * context-free call (dbw_grad_stats_static) on the calling thread. */
 const char* dbw_last_error(const dbw_ctx* ctx);
 
 /* Waits for the context's stream and reports device-side errors raised since
@@ -205,6 +207,31 @@ dbw_status dbw_aggregate_fastest(dbw_ctx* ctx, const float* G, const int64_t* ti
 dbw_status dbw_grad_stats(dbw_ctx* ctx, const float* G, const uint8_t* mask, int32_t k,
                           const float* g, const float* loss, float* sqnorm,
                           dbw_iter_stats* stats);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * statistics of dbw_grad_stats with no context, computed by the same kernels
+ * on the stream `stream` (a hipStream_t, NULL for the default stream) of the
+ * current device.  The call allocates nothing: its scratch (the selection
+ * list, n*ceil(P/256) per-row and 2*ceil(P/256) per-tile partial sums, each
+ * part rounded up to 256 bytes) lives in one file-scope device array of
+ * DBW_STATIC_SCRATCH_BYTES per GPU, held until the process ends.  G DEVICE
+ * float [n][P], mask DEVICE uint8 [n], g DEVICE float [P], loss DEVICE float
+ * [n]; writes sqnorm (DEVICE float [n]) and *stats (DEVICE dbw_iter_stats) as
+ * dbw_grad_stats does, except that for k = 1 V_plus is V_window (HOST, the
+ * caller's D-window mean of past V_plus).  A mask that does not hold exactly
+ * k ones yields NaN statistics.  Errors: DBW_EINVAL (n outside [1,
+ * DBW_MAX_N], P < 1, a NULL pointer, V_window not finite), DBW_ERANGE (k
+ * outside [1, n]), DBW_EUNSUPPORTED (P above 2^29, or a scratch need above
+ * DBW_STATIC_SCRATCH_BYTES), DBW_EHIP; dbw_last_error(NULL) then gives the
+ * text, per calling thread.  Every call on one GPU uses the same array: calls
+ * that overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller.  No part of the array needs clearing between calls
+ * (each value a call reads was written earlier in that call). */
+#define DBW_STATIC_SCRATCH_BYTES (8u * 1024u * 1024u)
+dbw_status dbw_grad_stats_static(int32_t n, int64_t P, const float* G, const uint8_t* mask, int32_t k,
+                                 const float* g, const float* loss, double V_window, float* sqnorm,
+                                 dbw_iter_stats* stats, void* stream);
 
 /* Choice of k_t = n - b_t from the context's estimator state (Sect. 3.3,
  * Eqs. gain, greedy, greedy2).  T_hat (DEVICE double [n]) holds the time

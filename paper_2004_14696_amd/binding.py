@@ -37,7 +37,9 @@ EXPORTED = (
     "dbw_samples_export", "dbw_samples_import", "dbw_profile_enable", "dbw_kernel_time",
     "dbw_profile_reset", "dbw_time_estimator_create", "dbw_time_estimator_destroy",
     "dbw_time_estimator_solve", "dbw_time_estimator_stats", "dbw_busy_export", "dbw_busy_import",
+    "dbw_grad_stats_static",
 )
+DBW_STATIC_SCRATCH_BYTES = 8 * 1024 * 1024
 
 
 class DBWError(RuntimeError):
@@ -132,6 +134,8 @@ def load_library(path: str = LIB_PATH):
     lib.dbw_kernel_time.restype = st
     lib.dbw_profile_reset.argtypes = [P]
     lib.dbw_profile_reset.restype = st
+    lib.dbw_grad_stats_static.argtypes = [c_int32, c_int64, P, P, c_int32, P, P, c_double, P, P, P]
+    lib.dbw_grad_stats_static.restype = st
     _lib = lib
     return lib
 
@@ -219,6 +223,40 @@ class TimeEstimator:
         if getattr(self, "h", None):
             self.lib.dbw_time_estimator_destroy(self.h)
             self.h = None
+
+
+def grad_stats_static(G, mask, k, g, loss, V_window=0.0, sqnorm=None, stats=None, stream=None):
+    """dbw_grad_stats_static: the statistics of dbw_grad_stats with no context
+    and no allocation inside the call (scratch in the library's static device
+    array).  G [n][P] float32, mask [n] uint8, g [P] float32, loss [n]
+    float32, all on the current device; V_window is V_plus for k = 1.
+    Returns (sqnorm [n] float32, stats float64 [4] = gnorm2, V_plus, N_plus,
+    F_hat); pass sqnorm and stats to write into existing tensors."""
+    torch = _torch()
+    lib = load_library()
+    if G.dim() != 2:
+        raise ValueError("G must be [n][P]")
+    n, P = G.shape
+    dev = G.device
+    for name, t, dtype, shape in (("G", G, torch.float32, (n, P)), ("mask", mask, torch.uint8, (n,)),
+                                  ("g", g, torch.float32, (P,)), ("loss", loss, torch.float32, (n,))):
+        if t.device != dev or t.dtype != dtype or not t.is_contiguous() or tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {shape} on {dev}")
+    sqnorm = torch.empty(n, dtype=torch.float32, device=dev) if sqnorm is None else sqnorm
+    stats = torch.empty(4, dtype=torch.float64, device=dev) if stats is None else stats
+    if tuple(sqnorm.shape) != (n,) or sqnorm.dtype != torch.float32 or sqnorm.device != dev:
+        raise ValueError("sqnorm must be float32 [n] on the device of G")
+    if tuple(stats.shape) != (4,) or stats.dtype != torch.float64 or stats.device != dev:
+        raise ValueError("stats must be float64 [4] on the device of G")
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    s = lib.dbw_grad_stats_static(int(n), int(P), c_void_p(G.data_ptr()), c_void_p(mask.data_ptr()), int(k),
+                                  c_void_p(g.data_ptr()), c_void_p(loss.data_ptr()), float(V_window),
+                                  c_void_p(sqnorm.data_ptr()), c_void_p(stats.data_ptr()),
+                                  c_void_p(stream.cuda_stream))
+    if s != DBW_OK:
+        raise DBWError(s, lib.dbw_last_error(None).decode())
+    return sqnorm, stats
 
 
 # ---------------------------------------------------------------------------

@@ -21,7 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdbw.so")
 
-SOURCES = ["dbw_api.cpp", "time_estimate.cpp", "k_ps.hip", "k_softmax.hip", "k_mlp.hip", "k_cnn.hip"]
+SOURCES = ["dbw_api.cpp", "time_estimate.cpp", "k_ps.hip", "k_softmax.hip", "k_mlp.hip", "k_cnn.hip",
+           "dbw_static.hip"]
 ARCH = "gfx950"
 COMMON = [
     "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-fvisibility=hidden",

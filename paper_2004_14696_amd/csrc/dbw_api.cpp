@@ -500,7 +500,21 @@ DBW_API int64_t dbw_param_count(const dbw_config* cfg) {
   return param_count(*cfg);
 }
 
-DBW_API const char* dbw_last_error(const dbw_ctx* ctx) { return ctx ? ctx->last_error.c_str() : "NULL context"; }
+namespace {
+thread_local std::string t_free_error = "no error";   // context-free calls of this thread
+}  // namespace
+
+dbw_status dbw::set_free_error(dbw_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  t_free_error = buf;
+  return s;
+}
+
+DBW_API const char* dbw_last_error(const dbw_ctx* ctx) { return ctx ? ctx->last_error.c_str() : t_free_error.c_str(); }
 
 DBW_API dbw_status dbw_create(const dbw_config* cfg, void* stream, dbw_ctx** out) {
   if (!out) return DBW_EINVAL;

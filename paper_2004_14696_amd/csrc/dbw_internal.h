@@ -200,13 +200,20 @@ struct FinalizeArgs {
   int n;
   float* sqnorm;        // [n]
   dbw_iter_stats* stats;
-  dbw_estimator_state* st;  // device; read (window mean), written if bookkeeping
+  dbw_estimator_state* st;  // device; read (window mean), written if bookkeeping;
+                            // nullable when bookkeeping is 0 and v_window_given is set
   double eta;
   int D;
   int bookkeeping;
-  int32_t* err;
+  int v_window_given;       // V_plus for k = 1 is v_window, not the state's window mean
+  double v_window;
+  int32_t* err;             // nullable: a mask count other than k then gives NaN statistics
 };
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
+
+// Error text of the context-free calls (per calling thread; dbw_last_error
+// with a NULL context returns it).  Returns s.
+dbw_status set_free_error(dbw_status s, const char* fmt, ...);
 
 // Mask -> arrival-order-free selection list (worker order) for the stats call.
 hipError_t launch_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel, int32_t* err,

@@ -265,7 +265,9 @@ __global__ __launch_bounds__(256) void k_mask_to_sel(const uint8_t* mask, int n,
       if (c < n) sel[c] = j;
       ++c;
     }
-  if (c != k) atomicOr(err, ERR_MASK_COUNT);
+  // fewer than k ones: the missing entries name no row (read as empty)
+  for (int r = c; r < k; ++r) sel[r] = -1;
+  if (c != k && err) atomicOr(err, ERR_MASK_COUNT);
 }
 
 // ---------------------------------------------------------------------------
@@ -658,7 +660,7 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
   }
   // block 0: statistics and estimator bookkeeping
   __shared__ dbw_estimator_state st;
-  load_state(a.st, &st);
+  if (a.st) load_state(a.st, &st);
   double m2 = 0.0, g2 = 0.0, ls = 0.0, cnt = 0.0;
   for (int64_t b = tid; b < a.nblocks; b += blockDim.x) {
     m2 += a.part[b * 2 + 0];
@@ -678,10 +680,13 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
     cnt = v[3];
   }
   if (tid == 0) {
-    if (static_cast<int>(cnt) != k) atomicOr(a.err, ERR_MASK_COUNT);
+    const bool count_ok = static_cast<int>(cnt) == k;
+    if (!count_ok && a.err) atomicOr(a.err, ERR_MASK_COUNT);
     double V_plus;
     if (k >= 2) {
       V_plus = m2 / (k - 1);
+    } else if (a.v_window_given) {
+      V_plus = a.v_window;
     } else {
       double s = 0.0;
       for (int i = 0; i < st.nV; ++i) s += st.hV[i];
@@ -689,10 +694,13 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
     }
     const double N_plus = fmax(g2 - V_plus / k, 0.0);
     const double F_hat = ls / k;
-    a.stats->gnorm2 = g2;
-    a.stats->V_plus = V_plus;
-    a.stats->N_plus = N_plus;
-    a.stats->F_hat = F_hat;
+    // without an error flag, a mask that does not hold k ones is reported
+    // through the statistics themselves
+    const double bad = !count_ok && !a.err ? NAN : 0.0;
+    a.stats->gnorm2 = g2 + bad;
+    a.stats->V_plus = V_plus + bad;
+    a.stats->N_plus = N_plus + bad;
+    a.stats->F_hat = F_hat + bad;
     if (a.bookkeeping) {
       const double eta = a.eta;
       if (st.t >= 1 && st.nV >= 1) {
