@@ -100,8 +100,13 @@ typedef enum { DBW_ESTIMATOR_ISOTONIC = 0, DBW_ESTIMATOR_NAIVE = 1 } dbw_estimat
  * directly, so the unselected rows are never formed and no row is read back;
  * g_t, the updated w, the losses, k and the mask are bitwise those of ALL,
  * the statistics equal up to the order of their fp64 and fp32 partial sums.
- * Rows not written hold unspecified values after dbw_step.  dbw_worker_grads
- * always writes every row. */
+ * Where the gradients come from per-worker GEMM tiles (softmax with more
+ * than 16 classes under SELECTED or NONE, the MLP and the CNN under
+ * SELECTED), the choice and the selection run before the gradient kernels,
+ * which compute every worker's gradient but store only the selected rows;
+ * k, the mask, g_t, w, the losses and the statistics are bitwise those of
+ * ALL.  Rows not written hold unspecified values after dbw_step.
+ * dbw_worker_grads always writes every row. */
 typedef enum { DBW_G_ROWS_ALL = 0, DBW_G_ROWS_SELECTED = 1, DBW_G_ROWS_NONE = 2 } dbw_g_rows;
 
 #define DBW_MAX_N 1024 /* logical workers per context                       */

@@ -15,6 +15,7 @@
 #include <limits>
 #include <mutex>
 #include <new>
+#include <optional>
 #include <string>
 #include <thread>
 #include <utility>
@@ -447,7 +448,7 @@ dbw_status sync_all(dbw_ctx* c) {
 }
 
 dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_t* y, const int32_t* rows,
-                        float* G, float* loss, bool keep_slabs = false) {
+                        float* G, float* loss, bool keep_slabs = false, const uint8_t* row_mask = nullptr) {
   ProfScope ps(c, DBW_KT_GRADS);
   const dbw_config& cf = c->cfg;
   hipError_t e;
@@ -459,6 +460,7 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.Gp = c->Gp; a.lossp = c->lossp; a.Z = c->Z; a.ce = c->ce;
     a.err = c->err;
     a.keep_slabs = keep_slabs ? 1 : 0;
+    a.row_mask = row_mask;
     e = dbw::launch_softmax_grads(c->splan, a, c->stream);
   } else if (cf.model == DBW_CNN) {
     dbw::CnnArgs a{};
@@ -468,14 +470,14 @@ dbw_status launch_grads(dbw_ctx* c, const float* w, const float* X, const int32_
     a.G = G; a.loss = loss;
     a.H1 = c->cH1; a.code1 = c->cCode1; a.F = c->cF; a.code2 = c->cCode2; a.ylab = c->cYlab;
     a.dP2 = c->cdP2; a.dP1 = c->cdP1; a.part1 = c->cPart1; a.part2 = c->cPart2; a.chunk = dbw::kCnnChunk;
-    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err;
+    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err; a.row_mask = row_mask;
     e = dbw::launch_cnn_grads(c->mplan, a, c->stream);
   } else {
     dbw::MlpArgs a{};
     a.w = w; a.X = X; a.y = y; a.rows = rows; a.S = cf.S;
     a.n = cf.n; a.B = cf.B; a.d = cf.d; a.H = cf.H; a.C = cf.C;
     a.G = G; a.loss = loss;
-    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err;
+    a.Hh = c->Hh; a.dA = c->dA; a.Gp = c->Gp; a.lossp = c->lossp; a.err = c->err; a.row_mask = row_mask;
     e = dbw::launch_mlp_grads(c->mplan, a, c->stream);
   }
   if (e != hipSuccess) return fail(c, DBW_EHIP, "gradient kernels: %s", hipGetErrorString(e));
@@ -799,14 +801,25 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   HostScope hs_step(c, DBW_KT_HOST_STEP);
   const int64_t t = c->t;
   const int slot = static_cast<int>(t % kSlots);
-  // 0. worker gradients on the context stream first: they need neither the
-  //    time estimate nor the choice, and keep the GPU busy while the host
-  //    waits for T_hat_t.  loss alternates halves by step parity (the
-  //    statistics of step t-1 may still read the other half).
+  // loss alternates halves by step parity (the statistics of step t-1 may
+  // still read the other half)
   float* loss = c->loss + (size_t)(t & 1) * n;
   //    With a slab source the partials stay for the PS kernel.
   const bool slab = c->slab_src != 0;
-  if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss, slab); s != DBW_OK) return s;
+  // Rows of G that nothing reads are skipped where the softmax gradients
+  // come from per-worker GEMM tiles (no slab source) and the choice is a
+  // kernel of its own: the choice and the selection then run first, and the
+  // gradient kernels store only the selected workers' rows (every gradient
+  // is still computed).  Otherwise the gradients go first: they need neither
+  // the time estimate nor the choice, and keep the GPU busy while the host
+  // waits for T_hat_t.  (The MLP and CNN kernels take the same row mask, but
+  // on their workloads the earlier choice cost more than the skipped rows
+  // saved, so their steps keep the gradients-first order.)
+  const bool mask_first = c->cfg.g_rows != DBW_G_ROWS_ALL && !slab && c->agg_nblocks > dbw::kStepPsMaxBlocks &&
+                          (c->cfg.model == DBW_SOFTMAX || c->cfg.g_rows == DBW_G_ROWS_SELECTED);
+  // 0. worker gradients first (see above)
+  if (!mask_first)
+    if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss, slab); s != DBW_OK) return s;
   // 1. T_hat_t in the pinned slot: solved by the worker since k_{t-2} became
   //    known, or here when no job was posted (first step of a history)
   {
@@ -846,7 +859,9 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
   //    context stream: the gradient kernel fills every CU, so nothing would
   //    run beside it)
   {
-    ProfScope ps(c, DBW_KT_AGGREGATE);
+    // with the choice first, its kernel is timed apart from the aggregation
+    std::optional<ProfScope> ps;
+    ps.emplace(c, mask_first ? DBW_KT_CHOOSE : DBW_KT_AGGREGATE);
     // k_t's pinned slot reads 0 until the PS kernel writes k_t (its previous
     // value, k_{t-4}, was read before the estimate of t-2)
     __atomic_store_n(c->h_k + slot, 0, __ATOMIC_RELEASE);
@@ -873,6 +888,13 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
       HIP_TRY(c, dbw::launch_step_ps(ca, aa, c->stream));
     } else {
       HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+    }
+    if (mask_first) {
+      // the selection is on the device: gradients with only the selected
+      // rows stored
+      ps.reset();
+      if (dbw_status s = launch_grads(c, w, X, y, rows, c->G, loss, false, c->mask); s != DBW_OK) return s;
+      ps.emplace(c, DBW_KT_AGGREGATE);
     }
     if (!fused) HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
     // T_hat_{t+1} on the worker now (it needs this iteration's ticks, stored

@@ -65,6 +65,7 @@ struct SoftmaxArgs {
   float* ce;             // [n*B] per-row CE (GEMM path)
   int32_t* err;
   int keep_slabs;        // 1: leave the slab partials for the PS kernel (no slab reduction)
+  const uint8_t* row_mask;  // nullable [n]: G rows only of workers with a nonzero entry
 };
 
 SoftmaxPlan softmax_plan(int n, int B, int d, int C);
@@ -88,6 +89,7 @@ struct MlpArgs {
   float* Gp;             // [n*slabs][H + H*C + C] head slab partials
   float* lossp;          // [n*slabs]
   int32_t* err;
+  const uint8_t* row_mask;  // nullable [n]: G rows only of workers with a nonzero entry
 };
 MlpPlan mlp_plan(int n, int B, int d, int H, int C);
 hipError_t launch_mlp_grads(const MlpPlan& plan, const MlpArgs& a, hipStream_t s);
@@ -124,6 +126,7 @@ struct CnnArgs {
   float* Gp;
   float* lossp;
   int32_t* err;
+  const uint8_t* row_mask;  // nullable [n]: G rows only of workers with a nonzero entry
 };
 int cnn_chunks(int B);
 hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t s);

@@ -688,7 +688,7 @@ __global__ __launch_bounds__(256) void k_cnn_wreduce(CnnArgs a, int chunks) {
   } else {
     for (int j = 0; j < chunks; ++j) s += a.part2[((int64_t)i * chunks + j) * L2 + (e - L1)];
   }
-  a.G[(int64_t)i * a.P + a.off_c1 + e] = s;
+  if (!a.row_mask || a.row_mask[i]) a.G[(int64_t)i * a.P + a.off_c1 + e] = s;
 }
 
 }  // namespace
@@ -708,7 +708,7 @@ hipError_t launch_cnn_grads(const MlpPlan& mplan, const CnnArgs& a, hipStream_t 
   m.w = a.w; m.X = a.F; m.y = a.ylab; m.rows = nullptr; m.S = 0;
   m.n = a.n; m.B = a.B; m.d = FEAT; m.H = a.H; m.C = a.C;
   m.G = a.G; m.ldG = a.P; m.loss = a.loss;
-  m.Hh = a.Hh; m.dA = a.dA; m.Gp = a.Gp; m.lossp = a.lossp; m.err = a.err;
+  m.Hh = a.Hh; m.dA = a.dA; m.Gp = a.Gp; m.lossp = a.lossp; m.err = a.err; m.row_mask = a.row_mask;
   e = launch_mlp_grads(mplan, m, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_cnn_dfeat, dim3((FEAT + 63) / 64, static_cast<unsigned>((nB + 63) / 64)), dim3(256), 0, s, a);

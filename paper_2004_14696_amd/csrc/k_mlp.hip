@@ -203,7 +203,7 @@ __global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a) {
 #pragma unroll
       for (int nt = 0; nt < WT; ++nt) {
         const int h = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
-        if (h < H) Gi[(int64_t)j * H + h] = acc[mt][nt][r];
+        if (h < H && (!a.row_mask || a.row_mask[i])) Gi[(int64_t)j * H + h] = acc[mt][nt][r];
       }
     }
 }
@@ -407,7 +407,7 @@ __global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int j = j0 + wm * 32 + mi * 16 + 4 * (lane / 16) + e;
-        if (j < d) Gi[(int64_t)j * H + nn] = acc[mi][ni][e];
+        if (j < d && (!a.row_mask || a.row_mask[i])) Gi[(int64_t)j * H + nn] = acc[mi][ni][e];
       }
     }
 }
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(256) void k_mlp_tail(MlpArgs a, int slabs, int64_t 
     const float* src = a.Gp + (int64_t)i * slabs * L + e;
     float s = 0.f;
     for (int q = 0; q < slabs; ++q) s += src[(int64_t)q * L];
-    a.G[(int64_t)i * P + (int64_t)a.d * a.H + e] = s;
+    if (!a.row_mask || a.row_mask[i]) a.G[(int64_t)i * P + (int64_t)a.d * a.H + e] = s;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     float s = 0.f;

@@ -200,16 +200,19 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
 __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
   __shared__ ChooseShared sh;
   __shared__ long long sh_t[DBW_MAX_N];
+  __shared__ int32_t sh_o[DBW_MAX_N];
   __shared__ int sh_cnt[16];
   const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
   const int n = a.n;
 
-  // stage the inputs (T_hat and ticks may live in pinned host memory); all
-  // loads are issued before their values are used
+  // stage the inputs (T_hat, ticks and the arrival order may live in pinned
+  // host memory); all loads are issued before their values are used
   if (a.do_choose) load_state(a.st, &sh.st);
+  const bool ordered = a.do_select && a.order_src;
   for (int i = tid; i < n; i += blockDim.x) {
     const double T = a.do_choose ? a.T_src[i] : 0.0;
     const long long t = a.do_select ? a.ticks_src[i] : 0;
+    const int32_t o = ordered ? a.order_src[i] : 0;
     if (a.do_choose) {
       sh.T[i] = T;
       if (a.T_hat) a.T_hat[i] = T;
@@ -218,6 +221,7 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
       sh_t[i] = t;
       if (a.ticks) a.ticks[i] = t;
     }
+    sh_o[i] = o;
   }
   __syncthreads();
 
@@ -234,13 +238,21 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
     for (int i = tid; i < n; i += blockDim.x) {
       const long long ti = sh_t[i];
       int rank = 0;
-      for (int j = 0; j < n; ++j) {
-        const long long tj = sh_t[j];
-        rank += (tj < ti) || (tj == ti && j < i);
+      if (ordered) {
+        // the host sorted the workers by (tick, index): position r holds
+        // the worker of rank r
+        const int wr = sh_o[i];
+        a.mask[wr] = i < k ? 1 : 0;
+        if (i < k) a.sel[i] = wr;
+      } else {
+        for (int j = 0; j < n; ++j) {
+          const long long tj = sh_t[j];
+          rank += (tj < ti) || (tj == ti && j < i);
+        }
+        const bool on = rank < k;
+        a.mask[i] = on ? 1 : 0;
+        if (on) a.sel[rank] = i;
       }
-      const bool on = rank < k;
-      a.mask[i] = on ? 1 : 0;
-      if (on) a.sel[rank] = i;
       finite += ti < INT64_MAX;
     }
 #pragma unroll
@@ -256,18 +268,24 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel,
-                                                     int32_t* err) {
-  if (threadIdx.x != 0) return;
+// One wave: the set mask entries in worker order, 64 at a time (ballot and
+// prefix popcount).
+__global__ __launch_bounds__(64) void k_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel,
+                                                    int32_t* err) {
+  const int lane = threadIdx.x;
+  const uint64_t below = (uint64_t{1} << lane) - 1;
   int c = 0;
-  for (int j = 0; j < n; ++j)
-    if (mask[j]) {
-      if (c < n) sel[c] = j;
-      ++c;
-    }
+  for (int base = 0; base < n; base += WAVE) {
+    const int j = base + lane;
+    const bool on = j < n && mask[j] != 0;
+    const uint64_t b = __builtin_amdgcn_ballot_w64(on);
+    const int r = c + __popcll(b & below);
+    if (on && r < n) sel[r] = j;
+    c += __popcll(b);
+  }
   // fewer than k ones: the missing entries name no row (read as empty)
-  for (int r = c; r < k; ++r) sel[r] = -1;
-  if (c != k && err) atomicOr(err, ERR_MASK_COUNT);
+  for (int r = c + lane; r < k; r += WAVE) sel[r] = -1;
+  if (lane == 0 && c != k && err) atomicOr(err, ERR_MASK_COUNT);
 }
 
 // ---------------------------------------------------------------------------

@@ -208,7 +208,7 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       const int j = tid + m * T;
-      if (j < d)
+      if (j < d && (!a.row_mask || a.row_mask[i]))
 #pragma unroll
         for (int c = 0; c < CP; ++c)
           if (c < C) a.G[(int64_t)i * P + (int64_t)j * C + c] = acc[m][c];
@@ -567,7 +567,8 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
     __syncthreads();
     const float4* s4 = reinterpret_cast<const float4*>(Ws);
     float4* o4 = reinterpret_cast<float4*>(a.G + (int64_t)i * P);
-    for (int k = tid; k < static_cast<int>(P / 4); k += MF_T) o4[k] = s4[k];
+    if (!a.row_mask || a.row_mask[i])
+      for (int k = tid; k < static_cast<int>(P / 4); k += MF_T) o4[k] = s4[k];
   }
   {
     // the loss of row w of each chunk sits in its label's lane of wave w
@@ -614,8 +615,9 @@ __global__ __launch_bounds__(256) void k_slab_reduce_tiles(SoftmaxArgs a, int sl
   const int f0 = x * 64;
   const int nf = min(64, d - f0);   // features past d are not stored
   float* dst = a.G + (int64_t)i * P + (int64_t)f0 * C;
-  for (int k = threadIdx.x; k < nf * C / 4; k += 256)
-    reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(tile)[k];
+  if (!a.row_mask || a.row_mask[i])
+    for (int k = threadIdx.x; k < nf * C / 4; k += 256)
+      reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(tile)[k];
   if (x == 0 && threadIdx.x == 0) {
     float l = 0.f;
     for (int q = 0; q < slabs; ++q) l += a.lossp[(int64_t)i * slabs + q];
@@ -632,7 +634,7 @@ __global__ __launch_bounds__(256) void k_slab_reduce(SoftmaxArgs a, int slabs) {
   const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   const float* src = a.Gp + (int64_t)i * slabs * P;
   float* dst = a.G + (int64_t)i * P;
-  if (e0 < P) {
+  if (e0 < P && (!a.row_mask || a.row_mask[i])) {
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(src, static_cast<uint32_t>(slabs * P * 4));
     float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
     if ((P & 3) == 0) {
@@ -806,7 +808,7 @@ __global__ __launch_bounds__(256) void k_grads_gemm(SoftmaxArgs a) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int nn = n0 + tx * 4 + c;
-      if (nn < C) a.G[(int64_t)i * P + (int64_t)j * C + nn] = acc[r][c];
+      if (nn < C && (!a.row_mask || a.row_mask[i])) a.G[(int64_t)i * P + (int64_t)j * C + nn] = acc[r][c];
     }
   }
   if (blockIdx.x == 0 && blockIdx.y == 0) {
@@ -887,6 +889,8 @@ __global__ __launch_bounds__(256) void k_grads_mfma(SoftmaxArgs a) {
   mfma_f32x4 acc[WT][WT];
   mfma_zero<WT>(acc);
   mfma_gemm_xt_r<WT>(L, xs, sh_row, d, j0, rs, B, C, n0, acc);
+  // the G rows of workers outside the row mask are computed but not stored
+  const bool write_g = !a.row_mask || a.row_mask[i];
 #pragma unroll
   for (int mt = 0; mt < WT; ++mt)
 #pragma unroll
@@ -896,7 +900,7 @@ __global__ __launch_bounds__(256) void k_grads_mfma(SoftmaxArgs a) {
 #pragma unroll
       for (int nt = 0; nt < WT; ++nt) {
         const int c = n0 + wn * 16 * WT + nt * 16 + (lane & 15);
-        if (c < C) a.G[(int64_t)i * P + (int64_t)j * C + c] = acc[mt][nt][r];
+        if (c < C && write_g) a.G[(int64_t)i * P + (int64_t)j * C + c] = acc[mt][nt][r];
       }
     }
   if (blockIdx.x == 0 && blockIdx.y == 0) {
@@ -924,7 +928,7 @@ constexpr int NARROW_MT = 2;
 // Z[m][c] = (softmax(x_m W)_c - [c = y_m]) / B, ce[m] = CE of row m;
 // blockIdx.x = tile of 64 MT rows.
 template <int MT, int NT>
-__global__ __launch_bounds__(256) void k_logits_softmax_mfma(SoftmaxArgs a) {
+__global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
   using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
   constexpr int BM = Lds::BM, BN = Lds::BN;
   constexpr int NPA = BM / 64;                          // A: BM rows x 4 float4
@@ -1031,14 +1035,13 @@ __global__ __launch_bounds__(256) void k_logits_softmax_mfma(SoftmaxArgs a) {
 // and all classes; blockIdx.x = feature tile, y = worker.  Block (0, i) also
 // writes loss_i.
 template <int MT, int NT>
-__global__ __launch_bounds__(256) void k_grads_mfma_n(SoftmaxArgs a) {
-  using Lds = MfmaLdsN<MT, NT, 64 * MT + 16>;
+__global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
+  using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
   constexpr int BM = Lds::BM, BN = Lds::BN;
   constexpr int NPA = BM / 64;                          // A: 16 rows x BM / 4 float4
   constexpr int NPB = (4 * BN + 255) / 256;             // B: 16 rows x BN / 4 float4
   __shared__ Lds L;
   __shared__ int sh_row[FUSED_MAX_ROWS];
-  __shared__ float sh[256];
   const int tid = threadIdx.x, lane = tid & 63, wm = tid >> 6;
   const int i = blockIdx.y;
   const int j0 = blockIdx.x * BM;
@@ -1081,7 +1084,9 @@ __global__ __launch_bounds__(256) void k_grads_mfma_n(SoftmaxArgs a) {
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  mfma_pipeline_n<MT, NT, 64 * MT + 16, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
+  mfma_pipeline_n<MT, NT, 64 * MT + 4, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
+  // the G rows of workers outside the row mask are computed but not stored
+  const bool write_g = !a.row_mask || a.row_mask[i];
   float* Gi = a.G + (int64_t)i * P;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -1092,11 +1097,13 @@ __global__ __launch_bounds__(256) void k_grads_mfma_n(SoftmaxArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int c = nt * 16 + (lane & 15);
-        if (c < C) Gi[(int64_t)j * C + c] = acc[mt][nt][r];
+        if (c < C && write_g) Gi[(int64_t)j * C + c] = acc[mt][nt][r];
       }
     }
   if (blockIdx.x == 0) {
-    // loss_i = mean CE over the worker's rows (fixed order)
+    // loss_i = mean CE over the worker's rows (fixed order), reduced in the
+    // LDS of the A tiles (free after the pipeline's last barrier)
+    float* sh = &L.A[0][0][0];
     float s = 0.f;
     for (int b = tid; b < B; b += 256) s += a.ce[(int64_t)i * B + b];
     sh[tid] = s;

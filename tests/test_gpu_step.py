@@ -143,6 +143,9 @@ def _lockstep(cfg, iters, seed_rows=False):
             _, _, dec = omodel.cnn_worker_grads(w_at, Xt, yt, cfg.H, cfg.C, return_preact=True)
         V_window = odbw.window_mean(orc.hV, cfg.D)
         rec = orc.step(Xt, yt, ticks)
+        # rows of G the GPU stored: every row, or (g_rows none on the paths
+        # whose gradient kernels take the selection) those of its selection
+        written = range(cfg.n) if cfg.g_rows == "all" else np.flatnonzero(host(out["mask"]))
         if cfg.model == "cnn":
             # pooling and ReLU choices within fp32 rounding may go either way:
             # each compared row's reference is the oracle with the subset of
@@ -151,7 +154,7 @@ def _lockstep(cfg, iters, seed_rows=False):
             # recomputed from these references with the oracle's functions
             Gg = host(out["G"]).astype(np.float64)
             Gref = rec["G"].copy()
-            for i in range(cfg.n):              # the CNN path writes every G row
+            for i in written:
                 deltas = cnn_flip_deltas(w_at, Xt[i], yt[i], cfg.H, cfg.C, dec[i], cnn_decision_flips(dec[i]))
                 err, Gref[i] = cnn_best_flip(Gg[i], rec["G"][i], deltas, cfg.H, cfg.C)
                 assert err <= RTOL, (cfg.name, t, i, len(deltas))
@@ -164,7 +167,7 @@ def _lockstep(cfg, iters, seed_rows=False):
             Gg = host(out["G"]).astype(np.float64)
             Gref = rec["G"].copy()
             tau = 1e-6 * float(np.max(np.abs(A)))
-            for i in range(cfg.n):                  # the MLP path writes every G row
+            for i in written:
                 flips = mlp_decision_flips(A[i], tau)
                 assert len(flips) <= max(16, A[i].size // 2000), (cfg.name, t, i, len(flips))   # rare
                 err, Gref[i] = mlp_best_flip(Gg[i], rec["G"][i],
@@ -374,6 +377,49 @@ def test_slab_aggregation_matches_row_aggregation(base):
         assert np.array_equal(Gs[sel], Ga[sel]), t
         unsel = np.setdiff1d(np.arange(cfg.n), sel)
         stale += sum(not np.array_equal(Gs[j], Ga[j]) for j in unsel)
+    assert stale > 0
+
+
+def test_lockstep_mlp_selected_rows():
+    # MLP with g_rows selected: the choice runs before the gradient kernels,
+    # which store only the selected workers' G rows
+    _lockstep(C4.replace(g_rows="selected"), 20)
+
+
+@pytest.mark.parametrize("base", [
+    C4,
+    C5.replace(name="C5small", n=8, B=64, S=2000),
+    C6.replace(name="C6small", n=4, B=16, S=800),
+], ids=lambda c: c.name)
+def test_skipped_rows_match_every_row(base):
+    # Gradients from per-worker GEMM tiles: with g_rows selected the choice
+    # and the selection run before the gradient kernels and only the
+    # selected rows of G are stored.  k, the mask, g, the update, the losses
+    # and the statistics are bitwise those of the run that stores every row;
+    # the selected rows of G are equal; the others keep stale values.
+    cfg = base.replace(policy="static", k_static=base.n // 2 + 1)
+    X, y = gen.dataset(cfg)
+    Xd, yd = to_dev(torch, X), to_dev(torch, y)
+    modes = ("all", "selected")
+    ctxs = {m: pb.Context(pb.config_from(cfg.replace(g_rows=m), S=cfg.S)) for m in modes}
+    ws = {m: to_dev(torch, init_params(cfg)) for m in modes}
+    stale = 0
+    for t in range(3):
+        rows = to_dev(torch, gen.batch_indices(cfg, t))
+        ticks = gen.round_trip_ticks(cfg, t)
+        ks = {m: ctxs[m].step(ws[m], Xd, yd, ticks, rows=rows, wait=True) for m in modes}
+        outs = {m: {k: host(v) for k, v in ctxs[m].step_outputs().items()} for m in modes}
+        for m in modes:
+            ctxs[m].sync()
+        ref, o = outs["all"], outs["selected"]
+        assert ks["selected"] == ks["all"] == cfg.k_static, t
+        for name in ("mask", "g", "loss", "k", "b", "T_hat", "stats", "sqnorm"):
+            assert np.array_equal(o[name], ref[name], equal_nan=True), (t, name)
+        assert np.array_equal(host(ws["selected"]), host(ws["all"])), t
+        sel = np.flatnonzero(ref["mask"])
+        assert np.array_equal(o["G"][sel], ref["G"][sel]), t
+        unsel = np.setdiff1d(np.arange(cfg.n), sel)
+        stale += sum(not np.array_equal(o["G"][j], ref["G"][j]) for j in unsel)
     assert stale > 0
 
 
