@@ -32,6 +32,12 @@ __device__ __forceinline__ float4 buf_f32x4(__amdgpu_buffer_rsrc_t r, uint32_t b
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
 }
 
+// The same with a wave-uniform byte offset soff added in the scalar operand
+// (no vector arithmetic per load; an out-of-range voff stays out of range).
+__device__ __forceinline__ float4 buf_f32x4_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, static_cast<int>(soff), 0));
+}
+
 __device__ __forceinline__ int32_t buf_i32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }

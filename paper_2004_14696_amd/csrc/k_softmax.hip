@@ -957,7 +957,29 @@ __global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
     const int64_t m = m0 + (tid + s2 * 256) / 4;
     xrow[s2] = m < Mrows ? sample_row(a, static_cast<int>(m / a.B), static_cast<int>(m % a.B), false) : -1;
   }
+  // byte offsets of this thread's pieces at k0 = 0 (out of range where the
+  // piece has no row or class); whole slices add k0 in the scalar offset
+  uint32_t aoff[NPA], boff[NPB];
+#pragma unroll
+  for (int s2 = 0; s2 < NPA; ++s2) {
+    const int kq = 4 * ((tid + s2 * 256) % 4);
+    aoff[s2] = xrow[s2] >= 0 ? static_cast<uint32_t>((xrow[s2] * d + kq) * 4) : kOutOfRange;
+  }
+#pragma unroll
+  for (int s2 = 0; s2 < NPB; ++s2) {
+    const int q = tid + s2 * 256;
+    const int kb = q / (BN / 4), nb = 4 * (q % (BN / 4));
+    boff[s2] = q < 4 * BN && nb < C ? static_cast<uint32_t>((kb * C + nb) * 4) : kOutOfRange;
+  }
   auto load = [&](int k0, float4 (&ra)[NPA], float4 (&rb)[NPB]) {
+    if (k0 + MBK <= d) {
+#pragma unroll
+      for (int s2 = 0; s2 < NPA; ++s2) ra[s2] = buf_f32x4_s(xs, aoff[s2], static_cast<uint32_t>(k0 * 4));
+#pragma unroll
+      for (int s2 = 0; s2 < NPB; ++s2) rb[s2] = buf_f32x4_s(ws, boff[s2], static_cast<uint32_t>(k0 * C * 4));
+      return;
+    }
+    // the last, partial slice: features past d read as 0
 #pragma unroll
     for (int s2 = 0; s2 < NPA; ++s2) {
       const int k = k0 + 4 * ((tid + s2 * 256) % 4);
@@ -1052,12 +1074,28 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.Z + (int64_t)i * B * C, static_cast<uint32_t>((int64_t)B * C * 4));
   for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(sample_row(a, i, b, false));
   __syncthreads();
+  // residual pieces: byte offsets at k0 = 0 (out of range past the classes);
+  // whole slices add k0 rows in the scalar offset
+  uint32_t boff[NPB];
+#pragma unroll
+  for (int s2 = 0; s2 < NPB; ++s2) {
+    const int q = tid + s2 * 256;
+    const int b = q / (BN / 4), c = 4 * (q % (BN / 4));
+    boff[s2] = q < 4 * BN && c < C ? static_cast<uint32_t>((b * C + c) * 4) : kOutOfRange;
+  }
   auto load = [&](int k0, float4 (&ra)[NPA], float4 (&rb)[NPB]) {
+    const bool whole = k0 + MBK <= B;
 #pragma unroll
     for (int s2 = 0; s2 < NPA; ++s2) {
       const int q = tid + s2 * 256;
       const int b = k0 + q / (BM / 4), j = j0 + 4 * (q % (BM / 4));
-      ra[s2] = buf_f32x4(xs, b < B && j < d ? static_cast<uint32_t>(((int64_t)sh_row[b] * d + j) * 4) : kOutOfRange);
+      ra[s2] = buf_f32x4(xs, (whole || b < B) && j < d ? static_cast<uint32_t>(((int64_t)sh_row[b] * d + j) * 4)
+                                                        : kOutOfRange);
+    }
+    if (whole) {
+#pragma unroll
+      for (int s2 = 0; s2 < NPB; ++s2) rb[s2] = buf_f32x4_s(rs, boff[s2], static_cast<uint32_t>(k0 * C * 4));
+      return;
     }
 #pragma unroll
     for (int s2 = 0; s2 < NPB; ++s2) {
