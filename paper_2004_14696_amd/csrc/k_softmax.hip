@@ -926,8 +926,9 @@ __global__ __launch_bounds__(256) void k_grads_mfma(SoftmaxArgs a) {
 constexpr int NARROW_MT = 2;
 
 // Z[m][c] = (softmax(x_m W)_c - [c = y_m]) / B, ce[m] = CE of row m;
-// blockIdx.x = tile of 64 MT rows.
-template <int MT, int NT>
+// blockIdx.x = tile of 64 MT rows.  RS > 0: C = 16 (NT - 1) + 4 RS, the last
+// tile in 4-wide stripes.
+template <int MT, int NT, int RS>
 __global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
   using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
   constexpr int BM = Lds::BM, BN = Lds::BN;
@@ -1014,7 +1015,7 @@ __global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  mfma_pipeline_n<MT, NT, 64 * MT + 4, NPA, NPB>(L, (d + MBK - 1) / MBK, load, store, acc);
+  mfma_pipeline_n<MT, NT, RS, 64 * MT + 4, NPA, NPB>(L, (d + MBK - 1) / MBK, load, store, acc);
 
   // row softmax: lane l holds rows 4 (l / 16) + r of each 16-row tile, class
   // 16 nt + l % 16; a row's classes are the 16 lanes of one DPP row
@@ -1055,8 +1056,8 @@ __global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
 
 // G_i[j][c] = sum_b X[row(i,b)][j] R_i[b][c] for a block of 64 MT features
 // and all classes; blockIdx.x = feature tile, y = worker.  Block (0, i) also
-// writes loss_i.
-template <int MT, int NT>
+// writes loss_i.  RS as for the logits.
+template <int MT, int NT, int RS>
 __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
   constexpr int BM = Lds::BM, BN = Lds::BN;
@@ -1122,7 +1123,7 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  mfma_pipeline_n<MT, NT, 64 * MT + 4, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
+  mfma_pipeline_n<MT, NT, RS, 64 * MT + 4, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
   // the G rows of workers outside the row mask are computed but not stored
   const bool write_g = !a.row_mask || a.row_mask[i];
   float* Gi = a.G + (int64_t)i * P;
@@ -1154,15 +1155,15 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   }
 }
 
-template <int NT>
+template <int NT, int RS>
 hipError_t launch_narrow_t(const SoftmaxArgs& a, hipStream_t s) {
   const int64_t Mrows = (int64_t)a.n * a.B;
   constexpr int BM = 64 * NARROW_MT;
-  hipLaunchKernelGGL((k_logits_softmax_mfma<NARROW_MT, NT>), dim3(static_cast<unsigned>((Mrows + BM - 1) / BM)),
+  hipLaunchKernelGGL((k_logits_softmax_mfma<NARROW_MT, NT, RS>), dim3(static_cast<unsigned>((Mrows + BM - 1) / BM)),
                      dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_grads_mfma_n<NARROW_MT, NT>), dim3(static_cast<unsigned>((a.d + BM - 1) / BM), a.n),
+  hipLaunchKernelGGL((k_grads_mfma_n<NARROW_MT, NT, RS>), dim3(static_cast<unsigned>((a.d + BM - 1) / BM), a.n),
                      dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -1173,14 +1174,26 @@ int narrow_tiles(int C, int d, int B) {
   return (C + 15) / 16;
 }
 
+template <int NT>
+hipError_t launch_narrow_nt(const SoftmaxArgs& a, hipStream_t s) {
+  // 4 or 8 classes in the last tile: 4-wide stripes (C = 16 (NT - 1) + 4 RS);
+  // with 12 the saving is small and the third stripe's registers are not
+  // free at 7 tiles, so a full tile is used
+  switch ((a.C % 16) / 4) {
+    case 1: return launch_narrow_t<NT, 1>(a, s);
+    case 2: return launch_narrow_t<NT, 2>(a, s);
+    default: return launch_narrow_t<NT, 0>(a, s);
+  }
+}
+
 hipError_t launch_narrow(const SoftmaxArgs& a, hipStream_t s) {
   switch (narrow_tiles(a.C, a.d, a.B)) {
-    case 2: return launch_narrow_t<2>(a, s);
-    case 3: return launch_narrow_t<3>(a, s);
-    case 4: return launch_narrow_t<4>(a, s);
-    case 5: return launch_narrow_t<5>(a, s);
-    case 6: return launch_narrow_t<6>(a, s);
-    case 7: return launch_narrow_t<7>(a, s);
+    case 2: return launch_narrow_nt<2>(a, s);
+    case 3: return launch_narrow_nt<3>(a, s);
+    case 4: return launch_narrow_nt<4>(a, s);
+    case 5: return launch_narrow_nt<5>(a, s);
+    case 6: return launch_narrow_nt<6>(a, s);
+    case 7: return launch_narrow_nt<7>(a, s);
   }
   return hipErrorInvalidValue;
 }

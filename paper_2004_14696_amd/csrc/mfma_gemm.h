@@ -162,6 +162,17 @@ __device__ __forceinline__ void mfma_gemm_xt_r(MfmaLds<WT>& L, __amdgpu_buffer_r
 // 16 x 16, so a block covers (64 MT) x (16 NT) outputs and the whole N extent
 // lives in one wave (N up to 16 NT: e.g. 100 classes in 7 tiles instead of a
 // 128-wide tile).  A rows are AST floats apart in LDS, B rows BST.
+//
+// With RS > 0 the last tile holds only 4 RS columns (N = 16 (NT - 1) + 4 RS)
+// and is computed as RS stripes of 4 columns on v_mfma_f32_4x4x1f32 (16
+// blocks of 4 x 4 x 1, 8 cycles) instead of a 16 x 16 x 4 product (32
+// cycles) that would be mostly padding.  Block b = 4 g + s of an instruction
+// takes rows 4 g .. 4 g + 3 of the 16-row tile at k offset s of the 4-deep
+// step (lane 4 b + i supplies A row i, lane 4 b + j B column j, and register i
+// of lane 4 b + j receives output (i, j)), so after the K loop a sum over the
+// four lanes of a 16-lane row that share lane % 4 (row rotations by 4 and 8)
+// leaves rows 4 (l / 16) + r, column 4 s + l % 4 of the stripe in register r:
+// the 16 x 16 tile layout, restricted to its first 4 RS columns.
 template <int MT, int NT, int AST>
 struct MfmaLdsN {
   static constexpr int BM = 64 * MT, BN = 16 * NT;
@@ -172,32 +183,72 @@ struct MfmaLdsN {
   float B[2][MBK][BST];
 };
 
-template <int MT, int NT, int AST>
+template <int MT, int NT, int RS, int AST>
 __device__ __forceinline__ void mfma_slice_n(const MfmaLdsN<MT, NT, AST>& L, int cbuf, int wm, int lane,
-                                             mfma_f32x4 (&acc)[MT][NT]) {
+                                             mfma_f32x4 (&acc)[MT][NT], mfma_f32x4 (&accs)[MT][RS > 0 ? RS : 1]) {
+  constexpr int NF = RS > 0 ? NT - 1 : NT;   // full 16-wide tiles
   const int i = lane & 15, kq = lane >> 4;
+  // stripe operands: k offset (lane / 4) % 4, row 4 (lane / 16) + lane % 4
+  const int ks4 = (lane >> 2) & 3, sr = 4 * (lane >> 4) + (lane & 3);
 #pragma unroll
   for (int ks = 0; ks < MBK; ks += 4) {
-    float av[MT], bv[NT];
+    float av[MT], bv[NF];
 #pragma unroll
     for (int t = 0; t < MT; ++t) av[t] = L.A[cbuf][ks + kq][wm * 16 * MT + t * 16 + i];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) bv[t] = L.B[cbuf][ks + kq][t * 16 + i];
+    for (int t = 0; t < NF; ++t) bv[t] = L.B[cbuf][ks + kq][t * 16 + i];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
+      for (int nt = 0; nt < NF; ++nt)
         acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+    if constexpr (RS > 0) {
+      float sa[MT], sb[RS];
+#pragma unroll
+      for (int t = 0; t < MT; ++t) sa[t] = L.A[cbuf][ks + ks4][wm * 16 * MT + t * 16 + sr];
+#pragma unroll
+      for (int s = 0; s < RS; ++s) sb[s] = L.B[cbuf][ks + ks4][NF * 16 + 4 * s + (lane & 3)];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int s = 0; s < RS; ++s) accs[mt][s] = __builtin_amdgcn_mfma_f32_4x4x1f32(sa[mt], sb[s], accs[mt][s], 0, 0, 0);
+    }
   }
+}
+
+// The four k-offset partials of a stripe summed (lanes 16 g + 4 s + j, s <
+// 4) and placed in the last tile's layout; columns past 4 RS read 0.
+template <int MT, int NT, int RS>
+__device__ __forceinline__ void mfma_fold_stripes(mfma_f32x4 (&acc)[MT][NT], mfma_f32x4 (&accs)[MT][RS]) {
+  const int sl = (threadIdx.x & 15) >> 2;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float out = 0.f;
+#pragma unroll
+      for (int s = 0; s < RS; ++s) {
+        float v = accs[mt][s][r];
+        v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false));
+        v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
+        out = sl == s ? v : out;
+      }
+      acc[mt][NT - 1][r] = out;
+    }
 }
 
 // The slice pipeline shared by the narrow-N GEMMs: load(k0, ra, rb) fetches
 // slice k0 into registers, store(buf, ra, rb) puts it into LDS buffer buf.
 // NPA / NPB float4 pieces per thread.
-template <int MT, int NT, int AST, int NPA, int NPB, class Load, class Store>
+template <int MT, int NT, int RS, int AST, int NPA, int NPB, class Load, class Store>
 __device__ __forceinline__ void mfma_pipeline_n(MfmaLdsN<MT, NT, AST>& L, int nk, Load load, Store store,
                                                 mfma_f32x4 (&acc)[MT][NT]) {
   const int lane = threadIdx.x & 63, wm = threadIdx.x >> 6;
+  mfma_f32x4 accs[MT][RS > 0 ? RS : 1];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int s = 0; s < (RS > 0 ? RS : 1); ++s) accs[mt][s] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
   float4 ra[NPA], rb[NPB];
   load(0, ra, rb);
   store(0, ra, rb);
@@ -205,10 +256,11 @@ __device__ __forceinline__ void mfma_pipeline_n(MfmaLdsN<MT, NT, AST>& L, int nk
   for (int kt = 0; kt < nk; ++kt) {
     const int cbuf = kt & 1;
     if (kt + 1 < nk) load((kt + 1) * MBK, ra, rb);
-    mfma_slice_n<MT, NT, AST>(L, cbuf, wm, lane, acc);
+    mfma_slice_n<MT, NT, RS, AST>(L, cbuf, wm, lane, acc, accs);
     if (kt + 1 < nk) store(cbuf ^ 1, ra, rb);
     __syncthreads();
   }
+  if constexpr (RS > 0) mfma_fold_stripes<MT, NT, RS>(acc, accs);
 }
 
 }  // namespace dbw

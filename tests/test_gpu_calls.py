@@ -46,6 +46,11 @@ SOFTMAX_SHAPES = [
     (9, 300, 512, 7),      # several row slabs per worker, ragged last slab
     (2, 10, 4500, 10),     # d beyond the fused kernel: GEMM path
     (4, 24, 300, 100),     # 100 classes: GEMM path on the matrix cores
+    (4, 70, 132, 20),      # one full class tile and one 4-wide stripe
+    (3, 45, 516, 24),      # one full tile and two stripes
+    (2, 130, 388, 52),     # three tiles and a stripe, ragged row tiles
+    (3, 33, 1000, 104),    # six tiles and two stripes
+    (2, 19, 260, 44),      # 12 classes in the last tile: a full tile
     (5, 33, 1000, 64),     # matrix-core GEMMs, ragged row tiles
     (3, 40, 260, 132),     # two class tiles
     (3, 70, 129, 17),      # GEMM path on the vector ALUs, ragged tiles
