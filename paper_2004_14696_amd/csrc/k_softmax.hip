@@ -291,7 +291,7 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
   constexpr int SL = 4 * U * CW + 2;
   constexpr int WS = MF_WAVES * 16 * SL;
   __shared__ __attribute__((aligned(16))) float Ws[WS];
-  __shared__ float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
+  __shared__ __attribute__((aligned(16))) float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
   __shared__ float rres[2][MF_ROWS][16];          // residuals of the chunk
   __shared__ float sloss[MF_WAVES];
   __shared__ int sh_row[FUSED_MAX_ROWS];

@@ -29,11 +29,13 @@ constexpr int MBK = 16, MPAD = 4;
 // blocks instead.
 constexpr int64_t kMfmaBigTiles = 512;
 
+// LDS arrays are 16-byte aligned so that float4 stores stay whole
+// (ds_write_b128, not two ds_write2_b32).
 template <int WT>
 struct MfmaLds {
   static constexpr int BM = 32 * WT;
-  float A[2][MBK][BM + MPAD];
-  float B[2][MBK][BM + MPAD];
+  __attribute__((aligned(16))) float A[2][MBK][BM + MPAD];
+  __attribute__((aligned(16))) float B[2][MBK][BM + MPAD];
 };
 
 template <int WT>
@@ -179,8 +181,8 @@ struct MfmaLdsN {
   // B rows 16 mod 64 floats apart: the four k rows of one read hit disjoint
   // bank quarters
   static constexpr int BST = (BN + 63) / 64 * 64 + 16;
-  float A[2][MBK][AST];
-  float B[2][MBK][BST];
+  __attribute__((aligned(16))) float A[2][MBK][AST];
+  __attribute__((aligned(16))) float B[2][MBK][BST];
 };
 
 template <int MT, int NT, int RS, int AST>
