@@ -81,6 +81,14 @@ def load_library(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2004_14696_amd.build`")
+    # torch carries its own HIP runtime; loaded first, it is the one the
+    # library binds to (loaded after the library, it would be a second
+    # runtime in the process, and device memory and streams would not be
+    # shared between the two)
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     st = c_int32
     P = c_void_p

@@ -885,7 +885,15 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     // is only taken within that bound)
     const bool fused = slab || c->agg_nblocks <= dbw::kStepPsMaxBlocks;
     if (fused) {
-      HIP_TRY(c, dbw::launch_step_ps(ca, aa, c->stream));
+      // small n: T_hat_t and the order travel in the kernel arguments
+      dbw::StepInline inl;
+      inl.n_inline = 0;
+      if (n <= dbw::kInlineN) {
+        std::memcpy(inl.T, c->h_T + (size_t)slot * n, sizeof(double) * n);
+        std::memcpy(inl.order, ho, sizeof(int32_t) * n);
+        inl.n_inline = n;
+      }
+      HIP_TRY(c, dbw::launch_step_ps(ca, aa, inl, c->stream));
     } else {
       HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
     }

@@ -190,7 +190,17 @@ hipError_t launch_aggregate(const AggArgs& a, hipStream_t s);
 // in one launch (dbw_step); ca.order_src must be set.  Used up to this many
 // column tiles (about two blocks per CU).
 constexpr int64_t kStepPsMaxBlocks = 512;
-hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, hipStream_t s);
+// T_hat and the arrival order passed in k_step_ps's kernel arguments when
+// n <= kInlineN (n_inline = n; 0: both are read from ca.T_src and
+// ca.order_src).  Every block reads them, so this replaces one read of
+// uncached pinned host memory per block by reads of the argument segment.
+constexpr int kInlineN = 64;
+struct StepInline {
+  double T[kInlineN];
+  int32_t order[kInlineN];
+  int n_inline;
+};
+hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, const StepInline& inl, hipStream_t s);
 
 struct FinalizeArgs {
   const float* sqpart;  // [n][nblocks]

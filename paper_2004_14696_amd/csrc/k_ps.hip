@@ -563,7 +563,7 @@ __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
 // (tiles follow the partial's layout, results land at their [d][C] column),
 // and block 0 also turns every worker's slab loss sums into its loss.
 template <bool VEC4, int SRC = SRC_ROWS, int S = 0>
-__global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca, AggArgs a) {
+__global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca, AggArgs a, StepInline inl) {
   constexpr int NW = STEP_PS_WAVES;
   // rows per wave and round: about 8 float4 loads in flight per lane within
   // the 128 registers a 16-wave block leaves each wave
@@ -582,9 +582,10 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
   int64_t wcol = col < a.P ? col : -1;
   if (SRC != SRC_ROWS) wcol = slab_column<SRC>(a, static_cast<int>(col));
   const float w_old = tid < AGG_TILE && wcol >= 0 && a.w ? a.w[wcol] : 0.f;
+  const bool given = inl.n_inline == n;
   for (int i = tid; i < n; i += blockDim.x) {
-    const double T = ca.T_src[i];
-    const int32_t o = ca.order_src[i];
+    const double T = given ? inl.T[i] : ca.T_src[i];
+    const int32_t o = given ? inl.order[i] : ca.order_src[i];
     const long long t = lead ? ca.ticks_src[i] : 0;
     cs.T[i] = T;
     sh_order[i] = o;
@@ -779,10 +780,11 @@ hipError_t launch_aggregate(const AggArgs& a, hipStream_t s) {
 }
 
 template <int SRC>
-void launch_step_ps_slabs(const ChooseArgs& ca, const AggArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+void launch_step_ps_slabs(const ChooseArgs& ca, const AggArgs& a, const StepInline& inl, dim3 grid, dim3 block,
+                          hipStream_t s) {
   switch (a.slabs) {
 #define DBW_SLABS_CASE(S) \
-    case S: hipLaunchKernelGGL((k_step_ps<true, SRC, S>), grid, block, 0, s, ca, a); return;
+    case S: hipLaunchKernelGGL((k_step_ps<true, SRC, S>), grid, block, 0, s, ca, a, inl); return;
     DBW_SLABS_CASE(2)
     DBW_SLABS_CASE(3)
     DBW_SLABS_CASE(4)
@@ -791,23 +793,24 @@ void launch_step_ps_slabs(const ChooseArgs& ca, const AggArgs& a, dim3 grid, dim
     DBW_SLABS_CASE(7)
     DBW_SLABS_CASE(8)
 #undef DBW_SLABS_CASE
-    default: hipLaunchKernelGGL((k_step_ps<true, SRC, 0>), grid, block, 0, s, ca, a);
+    default: hipLaunchKernelGGL((k_step_ps<true, SRC, 0>), grid, block, 0, s, ca, a, inl);
   }
 }
 
-hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, hipStream_t s) {
+hipError_t launch_step_ps(const ChooseArgs& ca, const AggArgs& a, const StepInline& inl, hipStream_t s) {
+  if (inl.n_inline != 0 && (inl.n_inline != ca.n || ca.n > kInlineN)) return hipErrorInvalidValue;
   const dim3 block(STEP_PS_WAVES * WAVE);
   if (a.src != SRC_ROWS) {
     // slab partials: float4 pieces of 4 consecutive elements
     if (a.slab_len % 4 != 0 || !a.Gp || !a.lossp || !a.loss || a.slabs < 1) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(agg_blocks(a.slab_len)));
-    if (a.src == SRC_SLAB_TILES) launch_step_ps_slabs<SRC_SLAB_TILES>(ca, a, grid, block, s);
-    else launch_step_ps_slabs<SRC_SLABS>(ca, a, grid, block, s);
+    if (a.src == SRC_SLAB_TILES) launch_step_ps_slabs<SRC_SLAB_TILES>(ca, a, inl, grid, block, s);
+    else launch_step_ps_slabs<SRC_SLABS>(ca, a, inl, grid, block, s);
     return hipGetLastError();
   }
   const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
-  if ((a.P % 4) == 0) hipLaunchKernelGGL(k_step_ps<true>, grid, block, 0, s, ca, a);
-  else hipLaunchKernelGGL(k_step_ps<false>, grid, block, 0, s, ca, a);
+  if ((a.P % 4) == 0) hipLaunchKernelGGL(k_step_ps<true>, grid, block, 0, s, ca, a, inl);
+  else hipLaunchKernelGGL(k_step_ps<false>, grid, block, 0, s, ca, a, inl);
   return hipGetLastError();
 }
 

@@ -197,6 +197,13 @@ def test_lockstep_tiny_teacher():
     assert len(set(orc.ks)) > 1    # the teacher labels make k move
 
 
+def test_lockstep_more_workers_than_inline_arguments():
+    # 80 workers: the fused PS kernel reads T_hat and the arrival order from
+    # pinned host memory (up to 64 they come in its kernel arguments)
+    orc = _lockstep(TINY.replace(name="tiny80", n=80, iters=30), 30)
+    assert len(set(orc.ks)) > 1
+
+
 def test_lockstep_4_workers_full_run():
     _lockstep(C1, C1.iters)
 
