@@ -318,7 +318,8 @@ def roofline_block(cfg, P: int, warm_ms: float, cold_ms: float, launches: int) -
 def ps_fixed_k(wl, G, Lb, reps: int = 10):
     """The aggregation call (dbw_aggregate_fastest: rank selection, then the
     k rows streamed once into g) and the statistics call (dbw_grad_stats:
-    mask to list, the k rows streamed against g, fixed-order finish) at
+    the k rows listed from the mask and streamed against g, fixed-order
+    finish) at
     fixed k = n and ceil(n/2) on the workload's gradient rows."""
     import torch
     ctx, cfg, P = wl.ctx, wl.cfg, wl.P

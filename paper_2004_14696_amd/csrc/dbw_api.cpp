@@ -758,9 +758,8 @@ DBW_API dbw_status dbw_grad_stats(dbw_ctx* c, const float* G, const uint8_t* mas
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
   ProfScope ps(c, DBW_KT_AGGREGATE);
-  HIP_TRY(c, dbw::launch_mask_to_sel(mask, c->cfg.n, k, c->sel, c->err, c->stream));
   dbw::AggArgs aa{};
-  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.sel = c->sel; aa.k_imm = k; aa.g_in = g;
+  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.sel_mask = mask; aa.k_imm = k; aa.g_in = g;
   aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_STATS_GIVEN_MEAN;
   HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
   dbw::FinalizeArgs fa{};

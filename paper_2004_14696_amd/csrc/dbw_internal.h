@@ -161,7 +161,8 @@ struct AggArgs {
   const float* G;       // [n][P]
   int64_t P;
   int n;
-  const int32_t* sel;   // arrival order; AGG_STATS_GIVEN_MEAN uses sel from the mask
+  const int32_t* sel;   // arrival order (AGG_MEAN, AGG_FUSED)
+  const uint8_t* sel_mask;  // AGG_STATS_GIVEN_MEAN: the selected rows, as a mask [n]
   const int32_t* k_dev; // nullable -> k_imm
   int k_imm;
   const float* g_in;    // AGG_STATS_GIVEN_MEAN
@@ -228,9 +229,6 @@ hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
 // with a NULL context returns it).  Returns s.
 dbw_status set_free_error(dbw_status s, const char* fmt, ...);
 
-// Mask -> arrival-order-free selection list (worker order) for the stats call.
-hipError_t launch_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel, int32_t* err,
-                              hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Host time estimator (exact constrained least squares).  An IsoSolver keeps

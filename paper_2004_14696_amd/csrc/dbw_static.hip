@@ -45,11 +45,11 @@ hipError_t scratch_on_current_device(void** out) {
 
 constexpr size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-// Scratch bytes of one call: the selection list [n], the per-row partial
-// squared norms [n][tiles] and the per-tile partial sums [tiles][2].
+// Scratch bytes of one call: the per-row partial squared norms [n][tiles]
+// and the per-tile partial sums [tiles][2].
 size_t scratch_bytes(int32_t n, int64_t P) {
   const size_t tiles = static_cast<size_t>(dbw::agg_blocks(P));
-  return align256(sizeof(int32_t) * n) + align256(sizeof(float) * n * tiles) + align256(2 * sizeof(double) * tiles);
+  return align256(sizeof(float) * n * tiles) + align256(2 * sizeof(double) * tiles);
 }
 
 }  // namespace
@@ -78,16 +78,13 @@ DBW_API dbw_status dbw_grad_stats_static(int32_t n, int64_t P, const float* G, c
     return set_free_error(DBW_EHIP, "dbw_grad_stats_static: address of the scratch array: %s", hipGetErrorString(e));
   const int64_t tiles = dbw::agg_blocks(P);
   unsigned char* p = static_cast<unsigned char*>(base);
-  int32_t* sel = reinterpret_cast<int32_t*>(p);
-  float* sqpart = reinterpret_cast<float*>(p + align256(sizeof(int32_t) * n));
-  double* part = reinterpret_cast<double*>(p + align256(sizeof(int32_t) * n) + align256(sizeof(float) * n * tiles));
+  float* sqpart = reinterpret_cast<float*>(p);
+  double* part = reinterpret_cast<double*>(p + align256(sizeof(float) * n * tiles));
   hipStream_t s = static_cast<hipStream_t>(stream);
   // every scratch value a kernel reads was written earlier in this call:
   // nothing needs clearing
-  if (dbw::launch_mask_to_sel(mask, n, k, sel, nullptr, s) != hipSuccess)
-    return set_free_error(DBW_EHIP, "dbw_grad_stats_static: launch failed");
   dbw::AggArgs aa{};
-  aa.G = G; aa.P = P; aa.n = n; aa.sel = sel; aa.k_imm = k; aa.g_in = g;
+  aa.G = G; aa.P = P; aa.n = n; aa.sel_mask = mask; aa.k_imm = k; aa.g_in = g;
   aa.sqpart = sqpart; aa.part = part; aa.mode = dbw::AGG_STATS_GIVEN_MEAN;
   if (dbw::launch_aggregate(aa, s) != hipSuccess)
     return set_free_error(DBW_EHIP, "dbw_grad_stats_static: launch failed");

@@ -33,18 +33,6 @@ constexpr int WAVE = 64;
 // most one round of row loads for k <= 64
 constexpr int STEP_PS_WAVES = 16;
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-  return v;
-}
-
-__device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-  return v;
-}
-
 // Lane exchange within rows of 16 lanes (xor 1, xor 2, half-row mirror, row
 // mirror): a butterfly whose four steps leave a row's combination in every
 // lane of the row.
@@ -75,6 +63,28 @@ __device__ __forceinline__ double row_sum_d(double v) {
   v += dpp_d<0x141>(v);
   v += dpp_d<0x140>(v);
   return v;
+}
+
+// Sums over the wave: a DPP butterfly in each 16-lane row, then the four
+// row sums read from lanes 0, 16, 32, 48 (fixed order; the same value in
+// every lane, on the vector ALUs with no LDS round trip).  Called with the
+// whole wave active.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += __builtin_bit_cast(float, dpp_i<0xB1>(__builtin_bit_cast(int, v)));
+  v += __builtin_bit_cast(float, dpp_i<0x4E>(__builtin_bit_cast(int, v)));
+  v += __builtin_bit_cast(float, dpp_i<0x141>(__builtin_bit_cast(int, v)));
+  v += __builtin_bit_cast(float, dpp_i<0x140>(__builtin_bit_cast(int, v)));
+  const int b = __builtin_bit_cast(int, v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+  v = row_sum_d(v);
+  return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
 }
 
 // Fixed-order sums of doubles over the block (blockDim.x a multiple of 64,
@@ -197,7 +207,7 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
 }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
+__global__ __launch_bounds__(1024) void k_choose_select(ChooseArgs a) {
   __shared__ ChooseShared sh;
   __shared__ long long sh_t[DBW_MAX_N];
   __shared__ int32_t sh_o[DBW_MAX_N];
@@ -235,25 +245,39 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
   if (a.do_select) {
     const int k = sh.kfinal;
     int finite = 0;
-    for (int i = tid; i < n; i += blockDim.x) {
-      const long long ti = sh_t[i];
-      int rank = 0;
-      if (ordered) {
-        // the host sorted the workers by (tick, index): position r holds
-        // the worker of rank r
-        const int wr = sh_o[i];
-        a.mask[wr] = i < k ? 1 : 0;
-        if (i < k) a.sel[i] = wr;
-      } else {
-        for (int j = 0; j < n; ++j) {
+    if (ordered) {
+      // the host sorted the workers by (tick, index): position r holds the
+      // worker of rank r
+      for (int r = tid; r < n; r += blockDim.x) {
+        const int wr = sh_o[r];
+        a.mask[wr] = r < k ? 1 : 0;
+        if (r < k) a.sel[r] = wr;
+        finite += sh_t[r] < INT64_MAX;
+      }
+    } else {
+      // rank of worker i by (tick, index): G consecutive lanes split the
+      // comparisons (G = 4 up to a quarter of the block's threads, then 2,
+      // then 1) and add their counts by quad DPP exchanges
+      const int nt = static_cast<int>(blockDim.x);
+      const int G = 4 * n <= nt ? 4 : 2 * n <= nt ? 2 : 1;
+      for (int t = tid; t < G * n; t += nt) {
+        const int i = t / G, q = t % G;
+        const long long ti = sh_t[i];
+        const int j1 = (q + 1) * n / G;
+        int rank = 0;
+        for (int j = q * n / G; j < j1; ++j) {
           const long long tj = sh_t[j];
           rank += (tj < ti) || (tj == ti && j < i);
         }
-        const bool on = rank < k;
-        a.mask[i] = on ? 1 : 0;
-        if (on) a.sel[rank] = i;
+        if (G >= 2) rank += dpp_i<0xB1>(rank);
+        if (G == 4) rank += dpp_i<0x4E>(rank);
+        if (q == 0) {
+          const bool on = rank < k;
+          a.mask[i] = on ? 1 : 0;
+          if (on) a.sel[rank] = i;
+          finite += ti < INT64_MAX;
+        }
       }
-      finite += ti < INT64_MAX;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) finite += __shfl_xor(finite, o, WAVE);
@@ -265,27 +289,6 @@ __global__ __launch_bounds__(256) void k_choose_select(ChooseArgs a) {
       if (k > total) atomicOr(a.err, ERR_K_RANGE);
     }
   }
-}
-
-// ---------------------------------------------------------------------------
-// One wave: the set mask entries in worker order, 64 at a time (ballot and
-// prefix popcount).
-__global__ __launch_bounds__(64) void k_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel,
-                                                    int32_t* err) {
-  const int lane = threadIdx.x;
-  const uint64_t below = (uint64_t{1} << lane) - 1;
-  int c = 0;
-  for (int base = 0; base < n; base += WAVE) {
-    const int j = base + lane;
-    const bool on = j < n && mask[j] != 0;
-    const uint64_t b = __builtin_amdgcn_ballot_w64(on);
-    const int r = c + __popcll(b & below);
-    if (on && r < n) sel[r] = j;
-    c += __popcll(b);
-  }
-  // fewer than k ones: the missing entries name no row (read as empty)
-  for (int r = c + lane; r < k; r += WAVE) sel[r] = -1;
-  if (lane == 0 && c != k && err) atomicOr(err, ERR_MASK_COUNT);
 }
 
 // ---------------------------------------------------------------------------
@@ -546,11 +549,49 @@ __device__ void aggregate_tile(const AggArgs& a, const int32_t* sel, int k, AggS
   agg_finish<VEC4, MODE, NW>(a, k, c, s1, s2, sh);
 }
 
+// The set entries of mask [n] in worker order into sel[0, k) (LDS), the
+// entries past their count -1 (no row; a count other than k is reported by
+// the statistics).  Ballots and prefix popcounts per wave, wave counts
+// through LDS; every thread of the block calls it.
+__device__ void mask_to_sel_block(const uint8_t* mask, int n, int k, int32_t* sel, int* sh_wc) {
+  const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
+  const int nw = static_cast<int>(blockDim.x) / WAVE;
+  const uint64_t below = (uint64_t{1} << lane) - 1;
+  int c = 0;
+  for (int base = 0; base < n; base += blockDim.x) {
+    const int j = base + tid;
+    const bool on = j < n && mask[j] != 0;
+    const uint64_t b = __builtin_amdgcn_ballot_w64(on);
+    if (lane == 0) sh_wc[wv] = __popcll(b);
+    __syncthreads();
+    int before = c, total = c;
+    for (int w = 0; w < nw; ++w) {
+      before += w < wv ? sh_wc[w] : 0;
+      total += sh_wc[w];
+    }
+    const int r = before + __popcll(b & below);
+    if (on && r < k) sel[r] = j;
+    c = total;
+    __syncthreads();
+  }
+  for (int r = c + tid; r < k; r += blockDim.x) sel[r] = -1;
+  __syncthreads();
+}
+
 template <bool VEC4, int MODE>
 __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
   __shared__ AggShared<AGG_WAVES> sh;
   const int k = a.k_dev ? a.k_dev[0] : a.k_imm;
-  aggregate_tile<VEC4, MODE, AGG_WAVES>(a, a.sel, k, sh);
+  if constexpr (MODE == AGG_STATS_GIVEN_MEAN) {
+    // the rows come as a mask: each block lists them itself (no separate
+    // launch; the list is n bytes of L2-resident reads per block)
+    __shared__ int32_t sh_sel[DBW_MAX_N];
+    __shared__ int sh_wc[AGG_WAVES];
+    mask_to_sel_block(a.sel_mask, a.n, k, sh_sel, sh_wc);
+    aggregate_tile<VEC4, MODE, AGG_WAVES>(a, sh_sel, k, sh);
+  } else {
+    aggregate_tile<VEC4, MODE, AGG_WAVES>(a, a.sel, k, sh);
+  }
 }
 
 // The PS side of one DBW iteration in one launch: every block makes the
@@ -751,17 +792,12 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
 }  // namespace
 
 hipError_t launch_choose_select(const ChooseArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_choose_select, dim3(1), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_mask_to_sel(const uint8_t* mask, int n, int k, int32_t* sel, int32_t* err,
-                              hipStream_t s) {
-  hipLaunchKernelGGL(k_mask_to_sel, dim3(1), dim3(64), 0, s, mask, n, k, sel, err);
+  hipLaunchKernelGGL(k_choose_select, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const AggArgs& a, hipStream_t s) {
+  if (a.mode == AGG_STATS_GIVEN_MEAN ? !a.sel_mask : !a.sel) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
   const dim3 block(AGG_WAVES * WAVE);
   const bool vec4 = (a.P % 4) == 0;
