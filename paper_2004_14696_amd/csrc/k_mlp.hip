@@ -494,7 +494,11 @@ hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& args, hipStream_t s
     default: return hipErrorNotSupported;
   }
   if (e != hipSuccess) return e;
-  if (big && (int64_t)((a.H + 127) / 128) * ((a.d + 127) / 128) * a.n >= kMfmaBigTiles)
+  // X_i^T dA_i contracts over the worker's B rows only: with few rows the
+  // large tile's operand reuse buys little, and the short blocks of 64 x 64
+  // tiles overlap one another's stores with their matrix work (MLP 32 x 64:
+  // 75.7 -> 73.0 us per launch)
+  if (big && a.B >= 256 && (int64_t)((a.H + 127) / 128) * ((a.d + 127) / 128) * a.n >= kMfmaBigTiles)
     hipLaunchKernelGGL(k_mlp_dw1_mfma<4>, dim3((a.H + 127) / 128, (a.d + 127) / 128, a.n), dim3(256), 0, s, a);
   else if (big)
     hipLaunchKernelGGL(k_mlp_dw1_mfma<2>, dim3((a.H + 63) / 64, (a.d + 63) / 64, a.n), dim3(256), 0, s, a);

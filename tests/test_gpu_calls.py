@@ -133,6 +133,7 @@ MLP_SHAPES = [
     (2, 5, 100, 300, 10),     # hidden width not a multiple of the block
     (3, 21, 260, 200, 10),    # matrix-core tiles, ragged in rows, features and units
     (16, 1000, 36, 512, 10),  # enough rows for 128 x 128 hidden-layer tiles
+    (8, 256, 1024, 1024, 10), # 256 rows per worker: 128 x 128 tiles for X_i^T dA_i
     (5, 13, 70, 600, 10),     # two hidden units per head thread
     (4, 9, 33, 17, 16),
     (1, 1, 3, 5, 2),
