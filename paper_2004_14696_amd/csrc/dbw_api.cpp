@@ -884,11 +884,13 @@ DBW_API dbw_status dbw_step(dbw_ctx* c, float* w, const float* X, const int32_t*
     // is only taken within that bound)
     const bool fused = slab || c->agg_nblocks <= dbw::kStepPsMaxBlocks;
     if (fused) {
-      // small n: T_hat_t and the order travel in the kernel arguments
+      // small n: T_hat_t, the ticks and the order travel in the kernel
+      // arguments
       dbw::StepInline inl;
       inl.n_inline = 0;
       if (n <= dbw::kInlineN) {
         std::memcpy(inl.T, c->h_T + (size_t)slot * n, sizeof(double) * n);
+        std::memcpy(inl.ticks, hk, sizeof(int64_t) * n);
         std::memcpy(inl.order, ho, sizeof(int32_t) * n);
         inl.n_inline = n;
       }

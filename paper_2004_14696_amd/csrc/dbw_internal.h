@@ -191,13 +191,15 @@ hipError_t launch_aggregate(const AggArgs& a, hipStream_t s);
 // in one launch (dbw_step); ca.order_src must be set.  Used up to this many
 // column tiles (about two blocks per CU).
 constexpr int64_t kStepPsMaxBlocks = 512;
-// T_hat and the arrival order passed in k_step_ps's kernel arguments when
-// n <= kInlineN (n_inline = n; 0: both are read from ca.T_src and
-// ca.order_src).  Every block reads them, so this replaces one read of
-// uncached pinned host memory per block by reads of the argument segment.
+// T_hat, the arrival order and the ticks passed in k_step_ps's kernel
+// arguments when n <= kInlineN (n_inline = n; 0: they are read from
+// ca.T_src, ca.order_src and ca.ticks_src).  Every block reads them, so this
+// replaces reads of uncached pinned host memory by reads of the argument
+// segment.
 constexpr int kInlineN = 64;
 struct StepInline {
   double T[kInlineN];
+  int64_t ticks[kInlineN];
   int32_t order[kInlineN];
   int n_inline;
 };

@@ -141,14 +141,22 @@ __device__ void choose_k(const ChooseArgs& a, ChooseShared& sh, bool write) {
   const dbw_estimator_state& st = sh.st;
   if (tid < WAVE) {
     // D-window means (oldest first, summed in order as the definition
-    // reads), the same sequence in every lane
+    // reads), the same sequence in every lane: lane i holds entry i (one
+    // LDS read per window, D <= 64), the additions run in order on lane
+    // reads instead of a chain of dependent LDS reads
+    const int nV = __builtin_amdgcn_readfirstlane(st.nV), nL = __builtin_amdgcn_readfirstlane(st.nL);
+    const double hv = lane < nV ? st.hV[lane] : 0.0;
+    const double hn = lane < nV ? st.hN[lane] : 0.0;
+    const double hl = lane < nL ? st.hL[lane] : 0.0;
     double V = 0.0, N = 0.0, L = 0.0;
-    for (int i = 0; i < st.nV; ++i) V += st.hV[i];
-    for (int i = 0; i < st.nV; ++i) N += st.hN[i];
-    for (int i = 0; i < st.nL; ++i) L += st.hL[i];
-    V = st.nV > 0 ? V / st.nV : 0.0;
-    N = st.nV > 0 ? N / st.nV : 0.0;
-    L = st.nL > 0 ? L / st.nL : 0.0;
+    for (int i = 0; i < nV; ++i) {
+      V += readlane_d(hv, i);
+      N += readlane_d(hn, i);
+    }
+    for (int i = 0; i < nL; ++i) L += readlane_d(hl, i);
+    V = nV > 0 ? V / nV : 0.0;
+    N = nV > 0 ? N / nV : 0.0;
+    L = nL > 0 ? L / nL : 0.0;
     const bool hasL = st.nL > 0;
     const double ga = a.eta - L * a.eta * a.eta / 2.0;
     const double gb = L * a.eta * a.eta / 2.0;
@@ -627,7 +635,7 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
   for (int i = tid; i < n; i += blockDim.x) {
     const double T = given ? inl.T[i] : ca.T_src[i];
     const int32_t o = given ? inl.order[i] : ca.order_src[i];
-    const long long t = lead ? ca.ticks_src[i] : 0;
+    const long long t = lead ? (given ? inl.ticks[i] : ca.ticks_src[i]) : 0;
     cs.T[i] = T;
     sh_order[i] = o;
     if (lead) {
