@@ -695,16 +695,6 @@ __global__ __launch_bounds__(STEP_PS_WAVES * WAVE) void k_step_ps(ChooseArgs ca,
 }
 
 // ---------------------------------------------------------------------------
-__device__ void push_window(double* h, int32_t* cnt, int D, double v) {
-  if (*cnt < D) {
-    h[*cnt] = v;
-    *cnt += 1;
-  } else {
-    for (int i = 0; i + 1 < D; ++i) h[i] = h[i + 1];
-    h[D - 1] = v;
-  }
-}
-
 __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
 #pragma clang fp contract(off)
   __shared__ double sh_red[64];
@@ -747,9 +737,18 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
     ls = v[2];
     cnt = v[3];
   }
-  if (tid == 0) {
+  if (tid < WAVE) {
+    // wave 0: every lane computes the same scalars (the same inputs and
+    // operations); lane i holds entry i of each D-window (D <= 64), so the
+    // window mean is one LDS read and in-order additions of lane reads, and
+    // a full window shifts by one in a single read and write
+    const int lane = tid;
+    const int nV = __builtin_amdgcn_readfirstlane(st.nV), nL = __builtin_amdgcn_readfirstlane(st.nL);
+    const double hv = lane < nV ? st.hV[lane] : 0.0;
+    const double hn = lane < nV ? st.hN[lane] : 0.0;
+    const double hl = lane < nL ? st.hL[lane] : 0.0;
     const bool count_ok = static_cast<int>(cnt) == k;
-    if (!count_ok && a.err) atomicOr(a.err, ERR_MASK_COUNT);
+    if (lane == 0 && !count_ok && a.err) atomicOr(a.err, ERR_MASK_COUNT);
     double V_plus;
     if (k >= 2) {
       V_plus = m2 / (k - 1);
@@ -757,38 +756,55 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
       V_plus = a.v_window;
     } else {
       double s = 0.0;
-      for (int i = 0; i < st.nV; ++i) s += st.hV[i];
-      V_plus = st.nV > 0 ? s / st.nV : 0.0;
+      for (int i = 0; i < nV; ++i) s += readlane_d(hv, i);
+      V_plus = nV > 0 ? s / nV : 0.0;
     }
     const double N_plus = fmax(g2 - V_plus / k, 0.0);
     const double F_hat = ls / k;
     // without an error flag, a mask that does not hold k ones is reported
     // through the statistics themselves
     const double bad = !count_ok && !a.err ? NAN : 0.0;
-    a.stats->gnorm2 = g2 + bad;
-    a.stats->V_plus = V_plus + bad;
-    a.stats->N_plus = N_plus + bad;
-    a.stats->F_hat = F_hat + bad;
+    if (lane == 0) {
+      a.stats->gnorm2 = g2 + bad;
+      a.stats->V_plus = V_plus + bad;
+      a.stats->N_plus = N_plus + bad;
+      a.stats->F_hat = F_hat + bad;
+    }
     if (a.bookkeeping) {
       const double eta = a.eta;
-      if (st.t >= 1 && st.nV >= 1) {
-        const double Nl = st.hN[st.nV - 1], Vl = st.hV[st.nV - 1];
+      const int D = a.D;
+      // append while the window is not full, else drop the oldest entry
+      // (lane i takes lane i + 1's) and put v last; returns the new count
+      auto push = [&](double* h, int cw, double held, double v) {
+        const double next = __shfl_down(held, 1, WAVE);
+        if (cw < D) {
+          if (lane == cw) h[lane] = v;
+          return cw + 1;
+        }
+        if (lane + 1 < D) h[lane] = next;
+        else if (lane + 1 == D) h[lane] = v;
+        return D;
+      };
+      int nL_new = nL;
+      if (st.t >= 1 && nV >= 1) {
+        const double Nl = readlane_d(hn, nV - 1), Vl = readlane_d(hv, nV - 1);
         const double den = eta * eta * (Nl + Vl / st.k_prev);
         if (den > 0.0) {
           const double Lp = 2.0 * (eta * Nl - (st.F_prev - F_hat)) / den;
-          push_window(st.hL, &st.nL, a.D, Lp);
+          nL_new = push(st.hL, nL, hl, Lp);
         }
       }
-      int32_t nv = st.nV;
-      push_window(st.hV, &nv, a.D, V_plus);
-      nv = st.nV;
-      push_window(st.hN, &nv, a.D, N_plus);
-      st.nV = nv;
-      st.F_prev2 = st.F_prev;
-      st.F_prev = F_hat;
-      st.nF = st.nF < 2 ? st.nF + 1 : 2;
-      st.k_prev = k;
-      st.t += 1;
+      const int nV_new = push(st.hV, nV, hv, V_plus);
+      (void)push(st.hN, nV, hn, N_plus);
+      if (lane == 0) {
+        st.nL = nL_new;
+        st.nV = nV_new;
+        st.F_prev2 = st.F_prev;
+        st.F_prev = F_hat;
+        st.nF = st.nF < 2 ? st.nF + 1 : 2;
+        st.k_prev = k;
+        st.t += 1;
+      }
     }
   }
   if (a.bookkeeping) {
