@@ -260,3 +260,37 @@ def test_incremental_estimator_on_push_and_wait_rows(lib):
     assert censored > iters          # the rows really are censored
     st = est.stats()
     assert st["full"] <= 1, st
+
+
+def test_estimator_push_and_wait_many_rows(lib):
+    # Push & Wait with k wandering over a wide range: the samples spread over
+    # many rows and the repairs re-partition components of hundreds of
+    # nodes, whose closures come from the grid program rather than a cut;
+    # exact against the stateless solver every iteration and the oracle
+    # every eighth.
+    from oracle.clock import PsWClock
+    rng = np.random.default_rng(48)
+    n, iters = 128, 40
+    clk = PsWClock(n)
+    cnt = np.zeros((n, n), np.int64)
+    tsum = np.zeros((n, n), np.int64)
+    est = pb.TimeEstimator()
+    h = n
+    for t in range(iters):
+        tau = np.rint((1 + rng.exponential(1.0, size=n)) * 2 ** 20).astype(np.int64)
+        k = int(rng.integers(4, 49))
+        samples, _ = clk.advance(clk.offsets(tau), k)
+        cnt[h - 1, :len(samples)] += 1
+        tsum[h - 1, :len(samples)] += samples
+        h = k
+        got = est.solve(cnt, tsum)
+        np.testing.assert_array_equal(got, pb.time_estimate(cnt, tsum))
+        if t % 8 == 7:
+            ref = te.time_estimate(cnt.tolist(), tsum.tolist())
+            for j in range(n):
+                if ref[j] is None:
+                    assert math.isnan(got[j])
+                else:
+                    assert got[j] == pytest.approx(ref[j], rel=1e-14, abs=0), (t, j)
+    assert int((cnt.sum(axis=1) > 0).sum()) >= 20     # many sampled rows
+    assert est.stats()["warm"] > 0
