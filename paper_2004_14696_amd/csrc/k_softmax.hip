@@ -1059,7 +1059,9 @@ __global__ __launch_bounds__(256, 4) void k_logits_softmax_mfma(SoftmaxArgs a) {
 // writes loss_i.  RS as for the logits.
 template <int MT, int NT, int RS>
 __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
-  using Lds = MfmaLdsN<MT, NT, 64 * MT + 4>;
+  // A rows 16 mod 64 floats apart: the four k rows of an operand read fall on
+  // disjoint bank quarters (the slice is stored as whole float4 rows)
+  using Lds = MfmaLdsN<MT, NT, 64 * MT + 16>;
   constexpr int BM = Lds::BM, BN = Lds::BN;
   constexpr int NPA = BM / 64;                          // A: 16 rows x BM / 4 float4
   constexpr int NPB = (4 * BN + 255) / 256;             // B: 16 rows x BN / 4 float4
@@ -1123,7 +1125,7 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-  mfma_pipeline_n<MT, NT, RS, 64 * MT + 4, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
+  mfma_pipeline_n<MT, NT, RS, 64 * MT + 16, NPA, NPB>(L, (B + MBK - 1) / MBK, load, store, acc);
   // the G rows of workers outside the row mask are computed but not stored
   const bool write_g = !a.row_mask || a.row_mask[i];
   float* Gi = a.G + (int64_t)i * P;
