@@ -208,6 +208,26 @@ __global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a) {
     }
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Max / sum over the 16 lanes of a DPP row: butterflies (xor 1, xor 2, half
+// mirror, mirror) that leave the identical value in every lane of the row.
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  return fmaxf(v, dpp<0x140>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  return v + dpp<0x140>(v);
+}
+
 // ---------------------------------------------------------------------------
 // Head: thread j < H owns hidden unit j (T == H rounded up to a wave multiple
 // is handled by the plan: T threads cover H with M units each).
@@ -247,24 +267,33 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
   const float invB = 1.0f / static_cast<float>(a.B);
   __syncthreads();
   const int64_t hrow0 = (int64_t)i * a.B;
-  for (int cb = 0; cb < nrows; cb += R) {
-    float x[R][M];
+  // rows cb .. cb + R - 1 as loaded: the activations, or with ksplit 2 the
+  // two K halves' sums (the second half sits in dA; this thread writes a
+  // row's dA entries only after it has read them).  The next rows are
+  // loaded one step ahead, so their latency overlaps a step's reductions.
+  auto load_rows = [&](int cb, float (&h1)[R][M], float (&h2)[R][M]) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const bool ok = cb + r < nrows;
       const int64_t hoff = (hrow0 + b0 + (ok ? cb + r : 0)) * H;
       const __amdgpu_buffer_rsrc_t hs = make_rsrc(a.Hh + hoff, ok ? static_cast<uint32_t>(H * 4) : 0u);
+      const __amdgpu_buffer_rsrc_t hd = make_rsrc(a.dA + hoff, ok && a.ksplit == 2 ? static_cast<uint32_t>(H * 4) : 0u);
 #pragma unroll
-      for (int m = 0; m < M; ++m) x[r][m] = buf_f32(hs, static_cast<uint32_t>((tid + m * T) * 4));
-      if (a.ksplit == 2) {
-        // the two K halves' sums (this row's dA entries are written later,
-        // by this same thread), the bias and the ReLU
-        const __amdgpu_buffer_rsrc_t h2 = make_rsrc(a.dA + hoff, ok ? static_cast<uint32_t>(H * 4) : 0u);
-#pragma unroll
-        for (int m = 0; m < M; ++m)
-          x[r][m] = fmaxf(x[r][m] + buf_f32(h2, static_cast<uint32_t>((tid + m * T) * 4)) + b1v[m], 0.f);
+      for (int m = 0; m < M; ++m) {
+        h1[r][m] = buf_f32(hs, static_cast<uint32_t>((tid + m * T) * 4));
+        h2[r][m] = buf_f32(hd, static_cast<uint32_t>((tid + m * T) * 4));
       }
     }
+  };
+  float h1[R][M], h2[R][M];
+  load_rows(0, h1, h2);
+  for (int cb = 0; cb < nrows; cb += R) {
+    float x[R][M];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < M; ++m) x[r][m] = a.ksplit == 2 ? fmaxf(h1[r][m] + h2[r][m] + b1v[m], 0.f) : h1[r][m];
+    if (cb + R < nrows) load_rows(cb + R, h1, h2);
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
@@ -276,11 +305,18 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
       }
     __syncthreads();
     if (tid < V * G) {
+      // four interleaved partial sums keep four LDS reads in flight
       const int v = tid % V, g = tid / V;
-      float s = 0.f;
-#pragma unroll 4
-      for (int t = g; t < T; t += G) s += red[t][v];
-      red2[g][v] = s;
+      float s4[4] = {0.f, 0.f, 0.f, 0.f};
+      int t = g;
+      for (; t + 3 * G < T; t += 4 * G) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) s4[u] += red[t + u * G][v];
+      }
+#pragma unroll
+      for (int u = 0; u < 3; ++u)
+        if (t + u * G < T) s4[u] += red[t + u * G][v];
+      red2[g][v] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
     }
     __syncthreads();
     if (tid < WAVE) {
@@ -293,14 +329,10 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
       }
       const bool valid = c < C;
       if (valid) z += bias2[c];
-      float zmax = valid ? z : -INFINITY;
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) zmax = fmaxf(zmax, __shfl_xor(zmax, o, 16));
+      const float zmax = row16_max(valid ? z : -INFINITY);
       const float sh = z - zmax;
       const float e = valid ? expf(sh) : 0.f;
-      float se = e;
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) se += __shfl_xor(se, o, 16);
+      const float se = row16_sum(e);
       const bool row_ok = rb < nrows;
       const int lab = row_ok ? sh_lab[rb] : 0;
       const float zy = __shfl(sh, r * 16 + lab, WAVE);
