@@ -35,6 +35,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
 FUSED_MAX_CLASSES = 16         # the single-pass softmax kernel covers C <= 16
 FLUSH_BYTES = 1 << 30          # touched between launches for the cold figures (MALL is 256 MB)
+SETTLE_S = 0.1                 # untimed gradient launches before the timed ones (clock settling)
 
 
 TRAFFIC_FILE = {
@@ -263,26 +264,43 @@ def time_steps(wl, warmup: int, steps: int, timing_pass: bool):
             "host": {k: v[0] / max(v[1], 1) for k, v in host.items()}, "k_last": st["k_prev"]}
 
 
-def time_grads(wl, first: int, steps: int):
-    """The worker-gradient call (dbw_worker_grads) alone: warm = back to back
-    between two events on the context stream; cold = each launch after a
-    1 GiB buffer was read (untimed), which evicts the 256 MB MALL and the
-    L2s without leaving dirty lines behind, with events around the launch
-    only."""
+def time_grads_warm(wl, first: int, steps: int, settle_s: float = SETTLE_S):
+    """The worker-gradient call (dbw_worker_grads) alone, warm: back to back
+    between two events on the context stream, after untimed launches that
+    keep the GPU busy for settle_s seconds (its clocks settle only after some
+    40 ms of sustained load; from idle the first launches of the 256 x 512
+    workload take 1.8 ms instead of 1.36).  Returns the mean launch time, the
+    settling launches and their seconds, and the output buffers."""
     import torch
     ctx, cfg = wl.ctx, wl.cfg
     G = torch.empty((cfg.n, wl.P), dtype=torch.float32, device=wl.dev)
     Lb = torch.empty(cfg.n, dtype=torch.float32, device=wl.dev)
-    ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first], G=G, loss=Lb)
+    settle = 0
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(4):
+            ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first + settle % steps], G=G, loss=Lb)
+            settle += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= settle_s:
+            break
+    settle_time = time.perf_counter() - t0
     g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     g0.record(ctx.stream)
     for t in range(steps):
         ctx.worker_grads(wl.w, wl.Xd, wl.yd, rows=wl.rows[first + t], G=G, loss=Lb)
     g1.record(ctx.stream)
     torch.cuda.synchronize()
-    warm_ms = g0.elapsed_time(g1) / steps
+    return g0.elapsed_time(g1) / steps, settle, settle_time, G, Lb
+
+
+def time_grads_cold(wl, first: int, steps: int, G, Lb):
+    """The same call cold: each launch after a 1 GiB buffer was read
+    (untimed), which evicts the 256 MB MALL and the L2s without leaving dirty
+    lines behind, with events around the launch only."""
+    import torch
+    ctx = wl.ctx
     flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=wl.dev)
-    cold = 0.0
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for t in range(steps):
         flush.sum()                   # read-only: no dirty lines left to write back
@@ -293,7 +311,7 @@ def time_grads(wl, first: int, steps: int):
     cold = sum(a.elapsed_time(b) for a, b in evs) / steps
     del flush
     ctx.sync()
-    return warm_ms, cold, G, Lb
+    return cold
 
 
 def roofline_block(cfg, P: int, warm_ms: float, cold_ms: float, launches: int) -> dict:
@@ -358,12 +376,19 @@ def measure(cfg, args, dev, with_ps: bool):
     total = args.warmup + 2 * args.steps + 1
     log(f"{cfg.name}: inputs")
     wl = Workload(cfg, dev, total)
+    # the gradient launches first: their untimed settling launches bring the
+    # GPU's clocks to their sustained level before the warm launches and the
+    # steps are timed
+    first = args.warmup + args.steps
+    log(f"{cfg.name}: gradient launches, settling and warm")
+    warm_ms, settle, settle_s, G, Lb = time_grads_warm(wl, first, args.steps)
     log(f"{cfg.name}: {args.warmup} + {args.steps} steps")
     st = time_steps(wl, args.warmup, args.steps, timing_pass=not args.no_kernel_timing)
-    first = args.warmup + args.steps
-    log(f"{cfg.name}: gradient launches, warm and cold")
-    warm_ms, cold_ms, G, Lb = time_grads(wl, first, args.steps)
+    log(f"{cfg.name}: gradient launches, cold")
+    cold_ms = time_grads_cold(wl, first, args.steps, G, Lb)
     res = {"step": st, "roofline": roofline_block(cfg, wl.P, warm_ms, cold_ms, args.steps), "P": wl.P}
+    res["roofline"]["settle"] = {"launches": settle, "s": settle_s,
+                                 "note": "untimed gradient launches before the warm launches and the steps"}
     if with_ps:
         log(f"{cfg.name}: aggregation and statistics at fixed k")
         res["ps_kernels"] = ps_fixed_k(wl, G, Lb)
