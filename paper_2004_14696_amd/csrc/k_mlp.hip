@@ -157,7 +157,10 @@ __global__ __launch_bounds__(256) void k_mlp_hidden_mfma(MlpArgs a) {
   // ReLU (two addends: the same sum in either order)
   const int kh = a.ksplit == 2 ? (d / 2 + MBK - 1) / MBK * MBK : d;
   const int kbeg = static_cast<int>(blockIdx.z) * kh;
-  mfma_gemm_rows_w<WT>(L, xs, xrow, d, ws, H, n0, acc, kbeg, min(d, kbeg + kh));
+  // two slices in flight: hidden layer 23.2 -> 22.0 us at 2048 x 784 x 512,
+  // 69.8 -> 61.9 us at 8000 x 800 x 500 (the X^T dA product, K = B, is
+  // slower that way and keeps one)
+  mfma_gemm_rows_w<WT, 2>(L, xs, xrow, d, ws, H, n0, acc, kbeg, min(d, kbeg + kh));
   const float* b1 = a.w + (int64_t)d * H;
   float* out = blockIdx.z == 0 ? a.Hh : a.dA;
 #pragma unroll

@@ -70,11 +70,47 @@ __device__ __forceinline__ void mfma_slice(const MfmaLds<WT>& L, int cbuf, int w
 template <int WT>
 constexpr int mfma_pieces() { return 32 * WT / 64; }
 
+// Block barrier once this wave's LDS reads and writes are complete; unlike
+// __syncthreads it does not wait for outstanding global loads, so slices
+// prefetched into registers stay in flight across it.
+__device__ __forceinline__ void mfma_lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt unconstrained
+  asm volatile("s_barrier" ::: "memory");
+}
+
+// The slice loop with PD slices in flight in registers: at step kt, register
+// slot kt % PD (whose slice is already in LDS) receives slice kt + PD, LDS
+// buffer kt & 1 is multiplied, and slot (kt + 1) % PD is stored into the
+// other buffer.  Loads past the last slice are issued anyway (the loaders
+// return 0 out of range), so the number of loads in flight is the same at
+// every step and the waits before the stores stay partial.
+template <int PD, int NP, class Load, class Store, class Slice>
+__device__ __forceinline__ void mfma_prefetch_loop(int nk, Load&& load, Store&& store, Slice&& slice) {
+  float4 ra[PD][NP], rb[PD][NP];
+#pragma unroll
+  for (int p = 0; p < PD; ++p) load(p * MBK, ra[p], rb[p]);
+  store(0, ra[0], rb[0]);
+  mfma_lds_barrier();
+  for (int kt0 = 0; kt0 < nk; kt0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      const int kt = kt0 + u;
+      if (kt < nk) {
+        load((kt + PD) * MBK, ra[u], rb[u]);
+        slice(kt & 1);
+        store((kt + 1) & 1, ra[(u + 1) % PD], rb[(u + 1) % PD]);
+        mfma_lds_barrier();
+      }
+    }
+  }
+}
+
 // acc += X[row(m0 + r)][k] W[k][n0 + c] over kbeg <= k < kend (default: all
 // K), for the block's tile.  xrow[s] is the dataset row of tile row
 // (tid + 256 s) / 4, or -1 for rows past the matrix; X rows have K floats;
-// W is K x N row-major (N % 4 == 0, K % 4 == 0, kbeg % 4 == 0).
-template <int WT>
+// W is K x N row-major (N % 4 == 0, K % 4 == 0, kbeg % 4 == 0).  PD > 1:
+// PD slices in flight (mfma_prefetch_loop).
+template <int WT, int PD = 1>
 __device__ __forceinline__ void mfma_gemm_rows_w(MfmaLds<WT>& L, __amdgpu_buffer_rsrc_t xs,
                                                  const int64_t (&xrow)[mfma_pieces<WT>()], int K,
                                                  __amdgpu_buffer_rsrc_t ws, int N, int n0, mfma_f32x4 (&acc)[WT][WT],
@@ -104,6 +140,11 @@ __device__ __forceinline__ void mfma_gemm_rows_w(MfmaLds<WT>& L, __amdgpu_buffer
       *reinterpret_cast<float4*>(&L.B[buf][q / BQ][4 * (q % BQ)]) = rb[s2];
     }
   };
+  if constexpr (PD > 1) {
+    mfma_prefetch_loop<PD, NP>((kend - kbeg + MBK - 1) / MBK, load, store,
+                               [&](int cbuf) { mfma_slice(L, cbuf, wm, wn, lane, acc); });
+    return;
+  }
   float4 ra[NP], rb[NP];
   load(0, ra, rb);
   store(0, ra, rb);
