@@ -1075,7 +1075,9 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
   const int64_t xrows = a.rows ? a.S : (int64_t)a.n * B;
   const __amdgpu_buffer_rsrc_t xs = make_rsrc(a.X, static_cast<uint32_t>(xrows * d * 4));
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.Z + (int64_t)i * B * C, static_cast<uint32_t>((int64_t)B * C * 4));
-  for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(sample_row(a, i, b, false));
+  // byte offsets of the worker's rows (the dataset is addressed by one buffer
+  // descriptor, below 2^31 bytes): no multiply per load
+  for (int b = tid; b < B; b += 256) sh_row[b] = static_cast<int>(sample_row(a, i, b, false) * d * 4);
   __syncthreads();
   // residual pieces: byte offsets at k0 = 0 (out of range past the classes);
   // whole slices add k0 rows in the scalar offset
@@ -1092,7 +1094,7 @@ __global__ __launch_bounds__(256, 4) void k_grads_mfma_n(SoftmaxArgs a) {
     for (int s2 = 0; s2 < NPA; ++s2) {
       const int q = tid + s2 * 256;
       const int b = k0 + q / (BM / 4), j = j0 + 4 * (q % (BM / 4));
-      ra[s2] = buf_f32x4(xs, (whole || b < B) && j < d ? static_cast<uint32_t>(((int64_t)sh_row[b] * d + j) * 4)
+      ra[s2] = buf_f32x4(xs, (whole || b < B) && j < d ? static_cast<uint32_t>(sh_row[b]) + static_cast<uint32_t>(j * 4)
                                                         : kOutOfRange);
     }
     if (whole) {
