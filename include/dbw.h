@@ -217,9 +217,9 @@ dbw_status dbw_grad_stats(dbw_ctx* ctx, const float* G, const uint8_t* mask, int
  * capture, tight serving loops, harnesses that forbid hipMalloc): the
  * statistics of dbw_grad_stats with no context, computed by the same kernels
  * on the stream `stream` (a hipStream_t, NULL for the default stream) of the
- * current device.  The call allocates nothing: its scratch (the selection
- * list, n*ceil(P/256) per-row and 2*ceil(P/256) per-tile partial sums, each
- * part rounded up to 256 bytes) lives in one file-scope device array of
+ * current device.  The call allocates nothing: its scratch (n*ceil(P/256)
+ * per-row float and 2*ceil(P/256) per-tile double partial sums, each part
+ * rounded up to 256 bytes) lives in one file-scope device array of
  * DBW_STATIC_SCRATCH_BYTES per GPU, held until the process ends.  G DEVICE
  * float [n][P], mask DEVICE uint8 [n], g DEVICE float [P], loss DEVICE float
  * [n]; writes sqnorm (DEVICE float [n]) and *stats (DEVICE dbw_iter_stats) as

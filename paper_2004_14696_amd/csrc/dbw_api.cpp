@@ -737,13 +737,11 @@ DBW_API dbw_status dbw_aggregate_fastest(dbw_ctx* c, const float* G, const int64
   if (k < 1 || k > c->cfg.n) return fail(c, DBW_ERANGE, "k=%d outside [1, %d]", k, c->cfg.n);
   DeviceGuard dg(c->device);
   ProfScope ps(c, DBW_KT_AGGREGATE);
-  dbw::ChooseArgs ca{};
-  ca.ticks_src = ticks; ca.n = c->cfg.n; ca.do_choose = 0; ca.do_select = 1; ca.k_imm = k;
-  ca.sel = c->sel; ca.mask = mask; ca.err = c->err;
-  HIP_TRY(c, dbw::launch_choose_select(ca, c->stream));
+  // one launch: every aggregation block ranks the n ticks itself and block 0
+  // writes the mask
   dbw::AggArgs aa{};
-  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.sel = c->sel; aa.k_imm = k; aa.g_out = g;
-  aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_MEAN;
+  aa.G = G; aa.P = c->P; aa.n = c->cfg.n; aa.ticks_sel = ticks; aa.mask_out = mask; aa.err = c->err;
+  aa.k_imm = k; aa.g_out = g; aa.sqpart = c->sqpart; aa.part = c->part; aa.mode = dbw::AGG_MEAN;
   HIP_TRY(c, dbw::launch_aggregate(aa, c->stream));
   return DBW_OK;
 }

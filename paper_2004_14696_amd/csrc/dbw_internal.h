@@ -162,6 +162,12 @@ struct AggArgs {
   int64_t P;
   int n;
   const int32_t* sel;   // arrival order (AGG_MEAN, AGG_FUSED)
+  // AGG_MEAN with ticks_sel set: every block takes the k fastest workers by
+  // (tick, index) itself (sel unused); block 0 writes mask_out [n] and
+  // reports k beyond the finite ticks in err
+  const int64_t* ticks_sel;
+  uint8_t* mask_out;
+  int32_t* err;
   const uint8_t* sel_mask;  // AGG_STATS_GIVEN_MEAN: the selected rows, as a mask [n]
   const int32_t* k_dev; // nullable -> k_imm
   int k_imm;

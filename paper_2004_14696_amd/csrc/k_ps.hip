@@ -586,11 +586,56 @@ __device__ void mask_to_sel_block(const uint8_t* mask, int n, int k, int32_t* se
   __syncthreads();
 }
 
-template <bool VEC4, int MODE>
+// The k fastest of n workers by (tick, index), listed in arrival order into
+// sel (LDS) by every block of an aggregation; block 0 also writes the mask
+// and reports k beyond the finite ticks.  Ranks are counts of the workers
+// ahead (the same comparisons as the selection kernel).
+__device__ void select_fastest_block(const int64_t* ticks, int n, int k, int32_t* sel, long long* sh_t,
+                                     uint8_t* mask, int32_t* err, int* sh_cnt) {
+  const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
+  const int nt = static_cast<int>(blockDim.x);
+  for (int i = tid; i < n; i += nt) sh_t[i] = ticks[i];
+  __syncthreads();
+  const bool lead = blockIdx.x == 0;
+  int finite = 0;
+  for (int i = tid; i < n; i += nt) {
+    const long long ti = sh_t[i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      const long long tj = sh_t[j];
+      rank += (tj < ti) || (tj == ti && j < i);
+    }
+    if (rank < k) sel[rank] = i;
+    if (lead) {
+      mask[i] = rank < k ? 1 : 0;
+      finite += ti < INT64_MAX;
+    }
+  }
+  if (lead) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) finite += __shfl_xor(finite, o, WAVE);
+    if (lane == 0) sh_cnt[wv] = finite;
+  }
+  __syncthreads();
+  if (lead && tid == 0) {
+    int total = 0;
+    for (int w = 0; w < nt / WAVE; ++w) total += sh_cnt[w];
+    if (k > total) atomicOr(err, ERR_K_RANGE);
+  }
+}
+
+template <bool VEC4, int MODE, bool SELECT = false>
 __global__ __launch_bounds__(AGG_WAVES * WAVE) void k_aggregate(AggArgs a) {
   __shared__ AggShared<AGG_WAVES> sh;
   const int k = a.k_dev ? a.k_dev[0] : a.k_imm;
-  if constexpr (MODE == AGG_STATS_GIVEN_MEAN) {
+  if constexpr (SELECT) {
+    // the selection in every block: no launch of its own before this one
+    __shared__ int32_t sh_sel[DBW_MAX_N];
+    __shared__ long long sh_t[DBW_MAX_N];
+    __shared__ int sh_cnt[AGG_WAVES];
+    select_fastest_block(a.ticks_sel, a.n, k, sh_sel, sh_t, a.mask_out, a.err, sh_cnt);
+    aggregate_tile<VEC4, MODE, AGG_WAVES>(a, sh_sel, k, sh);
+  } else if constexpr (MODE == AGG_STATS_GIVEN_MEAN) {
     // the rows come as a mask: each block lists them itself (no separate
     // launch; the list is n bytes of L2-resident reads per block)
     __shared__ int32_t sh_sel[DBW_MAX_N];
@@ -821,10 +866,17 @@ hipError_t launch_choose_select(const ChooseArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_aggregate(const AggArgs& a, hipStream_t s) {
-  if (a.mode == AGG_STATS_GIVEN_MEAN ? !a.sel_mask : !a.sel) return hipErrorInvalidValue;
+  const bool select = a.mode == AGG_MEAN && a.ticks_sel;
+  if (select ? !a.mask_out || !a.err : a.mode == AGG_STATS_GIVEN_MEAN ? !a.sel_mask : !a.sel)
+    return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(agg_blocks(a.P)));
   const dim3 block(AGG_WAVES * WAVE);
   const bool vec4 = (a.P % 4) == 0;
+  if (select) {
+    if (vec4) hipLaunchKernelGGL((k_aggregate<true, AGG_MEAN, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_aggregate<false, AGG_MEAN, true>), grid, block, 0, s, a);
+    return hipGetLastError();
+  }
 #define DBW_AGG_LAUNCH(V, M) hipLaunchKernelGGL((k_aggregate<V, M>), grid, block, 0, s, a)
   if (vec4) {
     if (a.mode == AGG_MEAN) DBW_AGG_LAUNCH(true, AGG_MEAN);
