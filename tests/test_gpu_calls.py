@@ -265,7 +265,8 @@ def test_worker_grads_cnn_rejects_other_image_sizes_and_reports_bad_rows_and_lab
 
 # -- aggregation --------------------------------------------------------------------
 
-@pytest.mark.parametrize("n,P", [(4, 7840), (16, 7840), (64, 30720), (5, 1001), (33, 259), (256, 4096)])
+@pytest.mark.parametrize("n,P", [(4, 7840), (16, 7840), (64, 30720), (5, 1001), (33, 259), (256, 4096),
+                                 (300, 1000), (1024, 260)])    # more workers than an aggregation block's threads
 def test_aggregate_fastest(n, P):
     rng = np.random.default_rng(n * 31 + P)
     G = rng.standard_normal((n, P)).astype(np.float32)
