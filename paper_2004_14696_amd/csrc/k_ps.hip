@@ -754,9 +754,19 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
       if (lane == 0) a.sqnorm[j] = 0.f;
       return;
     }
+    // the lane's entries in increasing order, eight loads in flight at a
+    // time (an unrolled loop would wait for each load before its addition)
     double s = 0.0;
     const float* p = a.sqpart + (int64_t)j * a.nblocks;
-    for (int64_t b = lane; b < a.nblocks; b += WAVE) s += p[b];
+    int64_t b = lane;
+    for (; b + 7 * WAVE < a.nblocks; b += 8 * WAVE) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[b + u * WAVE];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; b < a.nblocks; b += WAVE) s += p[b];
     s = wave_sum_d(s);
     if (lane == 0) a.sqnorm[j] = static_cast<float>(s);
     return;
@@ -765,9 +775,27 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
   __shared__ dbw_estimator_state st;
   if (a.st) load_state(a.st, &st);
   double m2 = 0.0, g2 = 0.0, ls = 0.0, cnt = 0.0;
-  for (int64_t b = tid; b < a.nblocks; b += blockDim.x) {
-    m2 += a.part[b * 2 + 0];
-    g2 += a.part[b * 2 + 1];
+  {
+    // in increasing tile order, four tiles' loads in flight at a time
+    const int64_t nt = blockDim.x;
+    int64_t b = tid;
+    for (; b + 3 * nt < a.nblocks; b += 4 * nt) {
+      double v[4][2];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v[u][0] = a.part[(b + u * nt) * 2 + 0];
+        v[u][1] = a.part[(b + u * nt) * 2 + 1];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        m2 += v[u][0];
+        g2 += v[u][1];
+      }
+    }
+    for (; b < a.nblocks; b += nt) {
+      m2 += a.part[b * 2 + 0];
+      g2 += a.part[b * 2 + 1];
+    }
   }
   for (int j = tid; j < a.n; j += blockDim.x)
     if (a.mask[j]) {
