@@ -755,18 +755,19 @@ __global__ __launch_bounds__(256) void k_finalize(FinalizeArgs a) {
       return;
     }
     // the lane's entries in increasing order, eight loads in flight at a
-    // time (an unrolled loop would wait for each load before its addition)
+    // time (a plain loop waits for each load before its addition); entries
+    // past the row read as 0, and adding +0 to these sums of squares (>= 0)
+    // changes no bit
     double s = 0.0;
-    const float* p = a.sqpart + (int64_t)j * a.nblocks;
-    int64_t b = lane;
-    for (; b + 7 * WAVE < a.nblocks; b += 8 * WAVE) {
+    const __amdgpu_buffer_rsrc_t p = make_rsrc(a.sqpart + (int64_t)j * a.nblocks,
+                                               static_cast<uint32_t>(a.nblocks * 4));
+    for (int64_t b = lane; b < a.nblocks; b += 8 * WAVE) {
       float v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = p[b + u * WAVE];
+      for (int u = 0; u < 8; ++u) v[u] = buf_f32(p, static_cast<uint32_t>((b + u * WAVE) * 4));
 #pragma unroll
       for (int u = 0; u < 8; ++u) s += v[u];
     }
-    for (; b < a.nblocks; b += WAVE) s += p[b];
     s = wave_sum_d(s);
     if (lane == 0) a.sqnorm[j] = static_cast<float>(s);
     return;
