@@ -15,6 +15,12 @@ features (32x32x3-shaped) and 100 classes, the largest of the five workloads
 bandwidth-bound workload (64 workers x 256 rows, 3072 features, 10 classes)
 that the metric's %-of-peak-HBM figure refers to, and under "ps_kernels" the
 aggregation and statistics calls at fixed k = n and ceil(n/2).
+
+Order per workload: 0.1 s of untimed gradient launches (the GPU's clocks
+settle only after some 40 ms of sustained load), the timed warm gradient
+launches ("roofline"), the W untimed and K timed steps, a second pass of K
+steps with per-launch events (the PS share), then the cold gradient launches
+(each after a 1 GiB read that evicts the MALL).
 """
 from __future__ import annotations
 
