@@ -7,7 +7,9 @@
 //  k_aggregate      streams the k selected gradient rows once: mean g_t
 //                   (Eq. grad_bw), per-column sums of squared deviations for
 //                   the variance estimate (Eq. sumvariancekt), per-row squared
-//                   norms, and optionally the SGD update (Eq. update).
+//                   norms, and optionally the SGD update (Eq. update).  For
+//                   the standalone mean every block ranks the ticks itself;
+//                   for the statistics every block lists the mask's rows.
 //  k_step_ps        the two above fused for dbw_step: every block repeats the
 //                   choice, the selection comes from the arrival order the
 //                   host sorted, and each block aggregates its column tile.
