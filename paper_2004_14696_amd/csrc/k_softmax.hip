@@ -57,6 +57,15 @@ __device__ __forceinline__ int sample_label(const SoftmaxArgs& a, int64_t row, b
   return lab;
 }
 
+// A label loaded by the caller, range-checked as in sample_label.
+__device__ __forceinline__ int checked_label(const SoftmaxArgs& a, int lab) {
+  if (lab < 0 || lab >= a.C) {
+    atomicOr(a.err, ERR_LABEL_RANGE);
+    return 0;
+  }
+  return lab;
+}
+
 // Block index -> logical (worker, slab) so that a worker's slabs run on the
 // same XCD (dispatch places block b on XCD b % 8): their partials then meet
 // in one L2.
@@ -242,14 +251,14 @@ __global__ __launch_bounds__(T) void k_softmax_fused(SoftmaxArgs a, int slabs, i
 // features, which sit on lane % 16) are computed on the vector ALUs: each
 // lane dots its 4U features of a row with W (staged once per block in LDS,
 // in lane order), a 16-lane DPP reduction sums the row group, and the eight
-// waves' partials meet in LDS.  Wave w then runs the softmax of row w of the
-// chunk (lane m = class) and the residuals meet in LDS again, so that lane
-// (m, g) reads r[row g + 4e][class m] -- the B operand of the same MFMAs.
-// Two block barriers per chunk.
+// waves' partials meet in LDS.  After one block barrier every wave sums the
+// partials of the rows its lanes hold and runs their softmax (16-lane DPP
+// max and sum), so lane (m, g) forms r[row g + 4e][class m] itself -- the
+// B operand of the same MFMAs.  One block barrier per chunk.
 constexpr int MF_WAVES = 8;
 constexpr int MF_T = MF_WAVES * WAVE;
 constexpr int MF_ROWS = 8;
-static_assert(MF_ROWS == MF_WAVES, "the softmax of a chunk gives one row to each wave");
+static_assert(MF_ROWS == 8, "lane (m, g) holds rows g and g + 4 of a chunk");
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
@@ -292,8 +301,6 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
   constexpr int WS = MF_WAVES * 16 * SL;
   __shared__ __attribute__((aligned(16))) float Ws[WS];
   __shared__ __attribute__((aligned(16))) float zb[2][MF_WAVES][MF_ROWS][16];  // per-wave partial logits
-  __shared__ float rres[2][MF_ROWS][16];          // residuals of the chunk
-  __shared__ float sloss[MF_WAVES];
   __shared__ int sh_row[FUSED_MAX_ROWS];
   __shared__ int sh_lab[FUSED_MAX_ROWS];
 
@@ -309,8 +316,18 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
   const int b0 = q * rps;
   const int nrows = min(a.B, b0 + rps) - b0;
 
-  // W in coalesced float4 pieces (P % 4 == 0 since d % 4 == 0), issued first
-  // so that their latency overlaps the row staging
+  // The chain to the first products is the row indices, then the rows: the
+  // indices are loaded first, then W (coalesced float4 pieces, P % 4 == 0
+  // since d % 4 == 0), then the labels, which are checked and staged only
+  // after the first rows are on their way (loads complete in issue order, so
+  // a label issued after the rows would wait for them).
+  constexpr int RPT = FUSED_MAX_ROWS / MF_T;   // slab rows per thread
+  int64_t rowv[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int r = tid + k * MF_T;
+    rowv[k] = r < nrows ? sample_row(a, i, b0 + r, true) : 0;
+  }
   const int n4 = static_cast<int>(P / 4);
   constexpr int KMAX = (MF_T * U * CW / 4 + MF_T - 1) / MF_T;   // P <= 512 U CW
   float4 wl[KMAX];
@@ -328,10 +345,15 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
     // of the same row)
     for (int k = tid; k < WS / 4; k += MF_T) w4[k] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  for (int r = tid; r < nrows; r += MF_T) {
-    const int64_t row = sample_row(a, i, b0 + r, true);
-    sh_row[r] = static_cast<int>(row);
-    sh_lab[r] = sample_label(a, row, true);
+  int labv[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int r = tid + k * MF_T;
+    labv[k] = 0;
+    if (r < nrows) {
+      sh_row[r] = static_cast<int>(rowv[k]);
+      labv[k] = a.y[rowv[k]];
+    }
   }
   __syncthreads();
 
@@ -361,6 +383,11 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
       xa[0][u] = load_u(r0, u);
       xa[1][u] = load_u(r1, u);
     }
+  }
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int r = tid + k * MF_T;
+    if (r < nrows) sh_lab[r] = checked_label(a, labv[k]);
   }
 
   // Stage W.  Features 4h .. 4h+3 (group h = w' 16U + 16u + m') are 4C
@@ -473,28 +500,29 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
       }
     }
   };
-  // After the barrier: the softmax of chunk cb's row w (lane m = class) from
-  // the eight waves' partials, residuals into rres, cross entropy into the
-  // label's lane; after a second barrier every lane takes its rows' residuals
-  // into rv.
+  // After the barrier: the softmax of the chunk's rows from the eight waves'
+  // partials, residuals into rv, cross entropy into the label's lane.
   auto softmax = [&](int cb, int buf) {
-    // wave w: row w of the chunk, lane m = class (the four row groups repeat it)
-    const int r = cb + w;
-    const bool row_ok = r < nrows;
-    float zt = 0.f;
+    // lane (m, g): rows g and g + 4 of the chunk, class m.  Every wave forms
+    // the residuals it needs from the eight waves' partials (the same
+    // arithmetic in every wave), so no second barrier; wave 0 keeps the
+    // cross entropy.
 #pragma unroll
-    for (int v = 0; v < MF_WAVES; ++v) zt += zb[buf][v][w][m];
-    float mx = row16_max(cls_ok ? zt : -INFINITY);
-    const float ex = cls_ok ? __expf(zt - mx) : 0.f;
-    const float se = row16_sum(ex);
-    const int lab = sh_lab[row_ok ? r : 0];
-    const bool hit = row_ok && m == lab;
-    const float p = ex * __builtin_amdgcn_rcpf(se);
-    if (g == 0) rres[buf][w][m] = row_ok && cls_ok ? (p - (hit ? 1.f : 0.f)) * invB : 0.f;
-    if (g == 0) loss_acc += hit ? __logf(se) - (zt - mx) : 0.f;
-    __syncthreads();
+    for (int e = 0; e < 2; ++e) {
+      const int r = cb + g + 4 * e;
+      const bool row_ok = r < nrows;
+      float zt = 0.f;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) rv[e] = rres[buf][g + 4 * e][m];
+      for (int v = 0; v < MF_WAVES; ++v) zt += zb[buf][v][g + 4 * e][m];
+      const float mx = row16_max(cls_ok ? zt : -INFINITY);
+      const float ex = cls_ok ? __expf(zt - mx) : 0.f;
+      const float se = row16_sum(ex);
+      const int lab = sh_lab[row_ok ? r : 0];
+      const bool hit = row_ok && m == lab;
+      const float p = ex * __builtin_amdgcn_rcpf(se);
+      rv[e] = row_ok && cls_ok ? (p - (hit ? 1.f : 0.f)) * invB : 0.f;
+      if (w == 0) loss_acc += hit ? __logf(se) - (zt - mx) : 0.f;
+    }
   };
   // One chunk: logits of chunk cb (rows in A) while chunk cb + 8 streams
   // into B, the block-wide softmax, then G += X^T R on the matrix cores.
@@ -570,18 +598,14 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
     if (!a.row_mask || a.row_mask[i])
       for (int k = tid; k < static_cast<int>(P / 4); k += MF_T) o4[k] = s4[k];
   }
-  {
-    // the loss of row w of each chunk sits in its label's lane of wave w
+  if (w == 0) {
+    // the loss of every row sits in its label's lane of wave 0
     float l = loss_acc;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
-    if (lane == 0) sloss[w] = l;
-    __syncthreads();
-    if (tid == 0) {
-      float t = 0.f;
-      for (int v = 0; v < MF_WAVES; ++v) t += sloss[v];
-      if (slabs == 1) a.loss[i] = t * invB;
-      else a.lossp[(int64_t)i * slabs + q] = t;
+    if (lane == 0) {
+      if (slabs == 1) a.loss[i] = l * invB;
+      else a.lossp[(int64_t)i * slabs + q] = l;
     }
   }
 }
