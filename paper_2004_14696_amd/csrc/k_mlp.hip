@@ -12,9 +12,9 @@
 //  k_mlp_head    per (worker, slab of rows): logits from Hh and W2 held in
 //                registers (thread = hidden unit), LDS reduction, softmax in
 //                wave 0, then dA rows and the slab partials of db1 | dW2 | db2.
-//  k_mlp_dw1     per worker: dW1 = X_i^T dA_i, fp32 MFMA GEMM, K = B.
-//  k_mlp_tail    sums the slab partials into G[i][d*H ...] (fixed order) and
-//                the loss.
+//  k_mlp_dw1     per worker: dW1 = X_i^T dA_i, fp32 MFMA GEMM, K = B; an
+//                extra grid row sums the head's slab partials into
+//                G[i][d*H ...] (fixed order) and the loss.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -41,14 +41,16 @@ __device__ __forceinline__ int64_t mlp_row(const MlpArgs& a, int i, int b, bool 
   return r;
 }
 
-__device__ __forceinline__ int mlp_label(const MlpArgs& a, int64_t row, bool report) {
-  const int lab = a.y[row];
+// A label loaded by the caller, range-checked (bad labels are reported and
+// read as class 0).
+__device__ __forceinline__ int checked_label(const MlpArgs& a, int lab) {
   if (lab < 0 || lab >= a.C) {
-    if (report) atomicOr(a.err, ERR_LABEL_RANGE);
+    atomicOr(a.err, ERR_LABEL_RANGE);
     return 0;
   }
   return lab;
 }
+
 
 // ---------------------------------------------------------------------------
 // MFMA tile: block 256 threads = 4 waves in 2 x 2, each wave 32 x 32 output
@@ -178,8 +180,40 @@ __global__ __launch_bounds__(256) void k_mlp_hidden_mfma(MlpArgs a) {
   }
 }
 
+// G[i][d*H + e] = sum_q Gp[i][q][e] for e < len (fixed slab order) and the
+// loss of worker i: the head's slab partials, summed by the extra grid row of
+// the dW1 kernels (part `part` of `nparts` blocks of 256 threads), which run
+// beside the X^T dA tiles and write a disjoint part of G.
+__device__ __forceinline__ void mlp_tail_sum(const MlpArgs& a, int slabs, int64_t len, int i, int part, int nparts) {
+  const int64_t P = a.ldG ? a.ldG : (int64_t)a.d * a.H + len;   // row stride of G
+  const bool keep = !a.row_mask || a.row_mask[i];
+  for (int64_t e = (int64_t)part * 256 + threadIdx.x; e < len; e += (int64_t)nparts * 256) {
+    const float* src = a.Gp + (int64_t)i * slabs * len + e;
+    float s = 0.f;
+    for (int q0 = 0; q0 < slabs; q0 += 8) {
+      // eight slabs' loads in flight, then added in slab order
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = q0 + u < slabs ? src[(int64_t)(q0 + u) * len] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (q0 + u < slabs) s += v[u];
+    }
+    if (keep) a.G[(int64_t)i * P + (int64_t)a.d * a.H + e] = s;
+  }
+  if (part == 0 && threadIdx.x == 0) {
+    float s = 0.f;
+    for (int q = 0; q < slabs; ++q) s += a.lossp[(int64_t)i * slabs + q];
+    a.loss[i] = s / static_cast<float>(a.B);
+  }
+}
+
 template <int WT>
-__global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a) {
+__global__ __launch_bounds__(256) void k_mlp_dw1_mfma(MlpArgs a, int slabs, int64_t tail) {
+  if (blockIdx.y == gridDim.y - 1) {
+    mlp_tail_sum(a, slabs, tail, static_cast<int>(blockIdx.z), static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x));
+    return;
+  }
   constexpr int BM = 32 * WT;
   __shared__ MfmaLds<WT> L;
   __shared__ int sh_row[1024];
@@ -250,25 +284,17 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
   const int tid = threadIdx.x;
   const int H = a.H, C = a.C, d = a.d;
   const int b0 = q * rps, b1 = min(a.B, b0 + rps), nrows = b1 - b0;
-  for (int r = tid; r < nrows; r += T) sh_lab[r] = mlp_label(a, mlp_row(a, i, b0 + r, false), true);
-  const float* W2 = a.w + (int64_t)d * H + H;
-  const float* bias2 = W2 + (int64_t)H * C;
-  const __amdgpu_buffer_rsrc_t w2s = make_rsrc(W2, static_cast<uint32_t>((int64_t)H * C * 4));
-  float wr[M][CP], gw2[M][CP], gb1[M], b1v[M];
+  // Nothing waits on the row indices but the labels, and nothing on the
+  // labels until the first softmax: the indices are loaded first, then the
+  // first rows and W2, then the labels, which are checked and staged in LDS
+  // before the first step's first barrier.
+  constexpr int LPT = (1024 + T - 1) / T;   // slab rows per thread
+  int64_t rowv[LPT];
 #pragma unroll
-  for (int m = 0; m < M; ++m) {
-    const int j = tid + m * T;
-    gb1[m] = 0.f;
-    b1v[m] = j < H ? a.w[(int64_t)d * H + j] : 0.f;
-#pragma unroll
-    for (int c = 0; c < CP; ++c) {
-      wr[m][c] = buf_f32(w2s, c < C ? static_cast<uint32_t>((j * C + c) * 4) : kOutOfRange);
-      gw2[m][c] = 0.f;
-    }
+  for (int k = 0; k < LPT; ++k) {
+    const int r = tid + k * T;
+    rowv[k] = r < nrows ? mlp_row(a, i, b0 + r, false) : 0;
   }
-  float loss_acc = 0.f, db2_acc = 0.f;
-  const float invB = 1.0f / static_cast<float>(a.B);
-  __syncthreads();
   const int64_t hrow0 = (int64_t)i * a.B;
   // rows cb .. cb + R - 1 as loaded: the activations, or with ksplit 2 the
   // two K halves' sums (the second half sits in dA; this thread writes a
@@ -290,6 +316,26 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
   };
   float h1[R][M], h2[R][M];
   load_rows(0, h1, h2);
+  const float* W2 = a.w + (int64_t)d * H + H;
+  const float* bias2 = W2 + (int64_t)H * C;
+  const __amdgpu_buffer_rsrc_t w2s = make_rsrc(W2, static_cast<uint32_t>((int64_t)H * C * 4));
+  float wr[M][CP], gw2[M][CP], gb1[M], b1v[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    const int j = tid + m * T;
+    gb1[m] = 0.f;
+    b1v[m] = j < H ? a.w[(int64_t)d * H + j] : 0.f;
+#pragma unroll
+    for (int c = 0; c < CP; ++c) {
+      wr[m][c] = buf_f32(w2s, c < C ? static_cast<uint32_t>((j * C + c) * 4) : kOutOfRange);
+      gw2[m][c] = 0.f;
+    }
+  }
+  float loss_acc = 0.f, db2_acc = 0.f;
+  const float invB = 1.0f / static_cast<float>(a.B);
+  int labv[LPT];
+#pragma unroll
+  for (int k = 0; k < LPT; ++k) labv[k] = tid + k * T < nrows ? a.y[rowv[k]] : 0;
   for (int cb = 0; cb < nrows; cb += R) {
     float x[R][M];
 #pragma unroll
@@ -306,6 +352,11 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
         for (int m = 0; m < M; ++m) z = fmaf(x[r][m], wr[m][c], z);
         red[tid][r * CP + c] = z;
       }
+    if (cb == 0) {
+#pragma unroll
+      for (int k = 0; k < LPT; ++k)
+        if (tid + k * T < nrows) sh_lab[tid + k * T] = checked_label(a, labv[k]);
+    }
     __syncthreads();
     if (tid < V * G) {
       // four interleaved partial sums keep four LDS reads in flight
@@ -372,23 +423,26 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
     if (c < CP) sh_db2[r][c] = db2_acc;
   }
   __syncthreads();
-  // slab partial, laid out like G's tail: [db1 (H) | dW2 (H x C) | db2 (C)]
-  float* gp = a.Gp + ((int64_t)i * slabs + q) * L;
+  // slab partial, laid out like G's tail: [db1 (H) | dW2 (H x C) | db2 (C)],
+  // assembled in the LDS of the reduction and written in 8-byte pieces (a
+  // thread's C classes are C floats apart from the next thread's)
+  static_assert(M * T + M * T * CP + CP <= T * (V + 1), "slab partial fits the reduction LDS");
+  float* stage = &red[0][0];
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     const int j = tid + m * T;
     if (j < H) {
-      gp[j] = gb1[m];
+      stage[j] = gb1[m];
 #pragma unroll
       for (int c = 0; c < CP; ++c)
-        if (c < C) gp[H + (int64_t)j * C + c] = gw2[m][c];
+        if (c < C) stage[H + j * C + c] = gw2[m][c];
     }
   }
   if (tid < C) {
     float s = 0.f;
 #pragma unroll
     for (int r = 0; r < R; ++r) s += sh_db2[r][tid];
-    gp[H + (int64_t)H * C + tid] = s;
+    stage[H + H * C + tid] = s;
   }
   if (tid == 0) {
     float s = 0.f;
@@ -396,10 +450,25 @@ __global__ __launch_bounds__(T) void k_mlp_head(MlpArgs a, int slabs, int rps, i
     for (int r = 0; r < R; ++r) s += sh_loss[r];
     a.lossp[(int64_t)i * slabs + q] = s;
   }
+  __syncthreads();
+  float* gp = a.Gp + ((int64_t)i * slabs + q) * L;
+  const int len = static_cast<int>(L);
+  if ((len & 1) == 0) {
+    // L even: every slab's partial starts 8-byte aligned
+    for (int k = tid; k < len / 2; k += T)
+      reinterpret_cast<float2*>(gp)[k] = make_float2(stage[2 * k], stage[2 * k + 1]);
+  } else {
+    for (int k = tid; k < len; k += T) gp[k] = stage[k];
+  }
 }
 
-// dW1[j][h] = sum_b X[row(i,b)][j] dA[i*B + b][h]; blockIdx.z = worker.
-__global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a) {
+// dW1[j][h] = sum_b X[row(i,b)][j] dA[i*B + b][h]; blockIdx.z = worker; the
+// last grid row sums the head's slab partials.
+__global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a, int slabs, int64_t tail) {
+  if (blockIdx.y == gridDim.y - 1) {
+    mlp_tail_sum(a, slabs, tail, static_cast<int>(blockIdx.z), static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x));
+    return;
+  }
   __shared__ float As[TK][TM + 4];
   __shared__ float Bs[TK][TN + 4];
   const int tid = threadIdx.x, lane = tid % WAVE, wv = tid / WAVE;
@@ -445,24 +514,6 @@ __global__ __launch_bounds__(256) void k_mlp_dw1(MlpArgs a) {
         if (j < d && (!a.row_mask || a.row_mask[i])) Gi[(int64_t)j * H + nn] = acc[mi][ni][e];
       }
     }
-}
-
-// G[i][d*H + e] = sum_q Gp[i][q][e] for e < L (fixed slab order); loss.
-__global__ __launch_bounds__(256) void k_mlp_tail(MlpArgs a, int slabs, int64_t L) {
-  const int i = blockIdx.y;
-  const int64_t P = a.ldG ? a.ldG : (int64_t)a.d * a.H + L;   // row stride of G
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e < L) {
-    const float* src = a.Gp + (int64_t)i * slabs * L + e;
-    float s = 0.f;
-    for (int q = 0; q < slabs; ++q) s += src[(int64_t)q * L];
-    if (!a.row_mask || a.row_mask[i]) a.G[(int64_t)i * P + (int64_t)a.d * a.H + e] = s;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    float s = 0.f;
-    for (int q = 0; q < slabs; ++q) s += a.lossp[(int64_t)i * slabs + q];
-    a.loss[i] = s / static_cast<float>(a.B);
-  }
 }
 
 template <int CP, int M, int T>
@@ -533,16 +584,16 @@ hipError_t launch_mlp_grads(const MlpPlan& p, const MlpArgs& args, hipStream_t s
   // large tile's operand reuse buys little, and the short blocks of 64 x 64
   // tiles overlap one another's stores with their matrix work (MLP 32 x 64:
   // 75.7 -> 73.0 us per launch)
+  // (one extra grid row sums the head's slab partials into the tail of G)
   if (big && a.B >= 256 && (int64_t)((a.H + 127) / 128) * ((a.d + 127) / 128) * a.n >= kMfmaBigTiles)
-    hipLaunchKernelGGL(k_mlp_dw1_mfma<4>, dim3((a.H + 127) / 128, (a.d + 127) / 128, a.n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_mlp_dw1_mfma<4>, dim3((a.H + 127) / 128, (a.d + 127) / 128 + 1, a.n), dim3(256), 0, s, a,
+                       p.slabs, p.tail);
   else if (big)
-    hipLaunchKernelGGL(k_mlp_dw1_mfma<2>, dim3((a.H + 63) / 64, (a.d + 63) / 64, a.n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_mlp_dw1_mfma<2>, dim3((a.H + 63) / 64, (a.d + 63) / 64 + 1, a.n), dim3(256), 0, s, a,
+                       p.slabs, p.tail);
   else
-    hipLaunchKernelGGL(k_mlp_dw1, dim3((a.H + TN - 1) / TN, (a.d + TM - 1) / TM, a.n), dim3(256), 0, s, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_mlp_tail, dim3(static_cast<unsigned>((p.tail + 255) / 256), a.n), dim3(256), 0, s, a,
-                     p.slabs, p.tail);
+    hipLaunchKernelGGL(k_mlp_dw1, dim3((a.H + TN - 1) / TN, (a.d + TM - 1) / TM + 1, a.n), dim3(256), 0, s, a,
+                       p.slabs, p.tail);
   return hipGetLastError();
 }
 
