@@ -118,7 +118,7 @@ def grads_kernels(cfg) -> str:
             return "k_logits_softmax_mfma + k_grads_mfma_n"
         return "k_logits_mfma + k_rows_softmax + k_grads_mfma"
     if cfg.model == "mlp":
-        return "k_mlp_hidden_mfma + k_mlp_head + k_mlp_dw1_mfma + k_mlp_tail"
+        return "k_mlp_hidden_mfma + k_mlp_head + k_mlp_dw1_mfma (with the head's slab sums)"
     return "k_cnn_* + MLP kernels on the 800 features"
 
 

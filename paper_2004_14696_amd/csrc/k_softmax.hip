@@ -626,9 +626,18 @@ __global__ __launch_bounds__(256) void k_slab_reduce_tiles(SoftmaxArgs a, int sl
     const int m = k % C, jg = k / C, g = jg % 4, j = jg / 4;
     const float* src = a.Gp + (int64_t)i * slabs * part + (int64_t)x * 64 * C + 4 * k;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int q = 0; q < slabs; ++q) {
-      const float4 v = *reinterpret_cast<const float4*>(src + q * part);
-      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    for (int q0 = 0; q0 < slabs; q0 += 8) {
+      // up to eight slabs' pieces in flight, then added in slab order (a
+      // plain loop over a run-time slab count waits for each load in turn)
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = q0 + u < slabs ? *reinterpret_cast<const float4*>(src + (q0 + u) * part) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (q0 + u < slabs) {
+          s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w;
+        }
     }
     tile[(16 * g + 0 + j) * C + m] = s.x;
     tile[(16 * g + 4 + j) * C + m] = s.y;
