@@ -682,11 +682,18 @@ __global__ __launch_bounds__(256) void k_cnn_wreduce(CnnArgs a, int chunks) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   constexpr int L1 = W1LEN + NC1, L2 = NC2 * K2 + NC2;
   if (e >= L1 + L2) return;
+  const float* src = e < L1 ? a.part1 + (int64_t)i * chunks * L1 + e : a.part2 + (int64_t)i * chunks * L2 + (e - L1);
+  const int64_t stride = e < L1 ? L1 : L2;
   float s = 0.f;
-  if (e < L1) {
-    for (int j = 0; j < chunks; ++j) s += a.part1[((int64_t)i * chunks + j) * L1 + e];
-  } else {
-    for (int j = 0; j < chunks; ++j) s += a.part2[((int64_t)i * chunks + j) * L2 + (e - L1)];
+  for (int j0 = 0; j0 < chunks; j0 += 8) {
+    // eight chunks' partials in flight, then added in chunk order (a plain
+    // loop over the run-time chunk count waits for each load in turn)
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = j0 + u < chunks ? src[(j0 + u) * stride] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (j0 + u < chunks) s += v[u];
   }
   if (!a.row_mask || a.row_mask[i]) a.G[(int64_t)i * a.P + a.off_c1 + e] = s;
 }
