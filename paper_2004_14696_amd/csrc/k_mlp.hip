@@ -51,7 +51,6 @@ __device__ __forceinline__ int checked_label(const MlpArgs& a, int lab) {
   return lab;
 }
 
-
 // ---------------------------------------------------------------------------
 // MFMA tile: block 256 threads = 4 waves in 2 x 2, each wave 32 x 32 output
 // (2 x 2 MFMA 16 x 16 tiles); K staged through LDS 16 at a time.

@@ -319,8 +319,8 @@ __global__ __launch_bounds__(MF_T) void k_softmax_mfma(SoftmaxArgs a, int slabs,
   // The chain to the first products is the row indices, then the rows: the
   // indices are loaded first, then W (coalesced float4 pieces, P % 4 == 0
   // since d % 4 == 0), then the labels, which are checked and staged only
-  // after the first rows are on their way (loads complete in issue order, so
-  // a label issued after the rows would wait for them).
+  // after the first rows are on their way (the wait for a load also waits
+  // for every load issued before it, so the labels go out before the rows).
   constexpr int RPT = FUSED_MAX_ROWS / MF_T;   // slab rows per thread
   int64_t rowv[RPT];
 #pragma unroll
