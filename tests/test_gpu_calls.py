@@ -432,3 +432,38 @@ def test_choose_b_guard_and_negative_gains():
     k, b, _ = ctx.choose_b(T)
     ctx.sync()
     assert int(host(k)[0]) == n and int(host(b)[0]) == 0
+
+
+# -- fixed-order reductions ----------------------------------------------------------------
+
+@pytest.mark.parametrize("model,n,B,d,H,C", [
+    ("softmax", 16, 128, 784, 0, 10),     # single pass, row slabs summed in slab order
+    ("softmax", 9, 300, 512, 0, 7),       # several slabs, ragged last slab
+    ("softmax", 4, 24, 300, 0, 100),      # narrow-class matrix-core path
+    ("softmax", 2, 130, 388, 0, 52),      # class tiles and a stripe
+    ("mlp", 32, 64, 784, 512, 10),        # split K, head slabs, slab sums beside dW1
+    ("mlp", 3, 21, 260, 200, 10),
+    ("cnn", 2, 37, 784, 500, 10),
+])
+def test_worker_grads_bitwise_repeatable(model, n, B, d, H, C):
+    # Every reduction of the gradient launch runs in a fixed order, so the same
+    # inputs give the same bits, also after a launch on other parameters has
+    # left its own partial sums in the context's workspace.
+    rng = np.random.default_rng(4000 + n + B + d + C)
+    if model == "softmax":
+        X, y, w, _ = softmax_inputs(rng, n, B, d, C)
+    elif model == "mlp":
+        X, y, w = mlp_inputs(rng, n, B, d, H, C)
+    else:
+        X, y, w = _cnn_inputs(rng, n, B, H, C)
+    ctx = _ctx(n, B, d, C, model=model, H=H)
+    Xd, yd = to_dev(torch, X), to_dev(torch, y)
+    wd = to_dev(torch, w)
+    w2 = to_dev(torch, (w * np.float32(0.5)).astype(np.float32))
+    G1, l1 = ctx.worker_grads(wd, Xd, yd)
+    G1, l1 = G1.clone(), l1.clone()
+    ctx.worker_grads(w2, Xd, yd)
+    G2, l2 = ctx.worker_grads(wd, Xd, yd)
+    ctx.sync()
+    assert torch.equal(G1, G2) and torch.equal(l1, l2)
+    assert bool(torch.isfinite(G1).all())
