@@ -233,6 +233,11 @@ __device__ __forceinline__ void mfma_slice_n(const MfmaLdsN<MT, NT, AST>& L, int
   const int i = lane & 15, kq = lane >> 4;
   // stripe operands: k offset (lane / 4) % 4, row 4 (lane / 16) + lane % 4
   const int ks4 = (lane >> 2) & 3, sr = 4 * (lane >> 4) + (lane & 3);
+  // A wave issuing its slice's products is given issue priority over the
+  // SIMD's other waves (their loads and LDS stores wait a little), so the
+  // matrix pipe is refilled sooner: 1316 -> 1308 us on the 256 x 512 x 3072
+  // x 100 launch (mean of eight paired runs).
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int ks = 0; ks < MBK; ks += 4) {
     float av[MT], bv[NF];
@@ -257,6 +262,7 @@ __device__ __forceinline__ void mfma_slice_n(const MfmaLdsN<MT, NT, AST>& L, int
         for (int s = 0; s < RS; ++s) accs[mt][s] = __builtin_amdgcn_mfma_f32_4x4x1f32(sa[mt], sb[s], accs[mt][s], 0, 0, 0);
     }
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // The four k-offset partials of a stripe summed (lanes 16 g + 4 s + j, s <
